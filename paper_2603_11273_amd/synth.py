@@ -1,0 +1,296 @@
+"""Seeded synthetic inputs for the batched Whisper-shaped ASR step.
+
+This module is shared by the oracle tests, the GPU parity tests and the
+benchmark.  It holds none of the method's arithmetic: it only draws data with
+the shapes and distributions of the paper's workloads (Section 4, setup:
+LibriSpeech-like right-skewed durations, a flat synthetic duration split,
+Poisson arrivals) and the Whisper-shaped model sizes the build is measured on.
+
+Two kinds of generator live here.
+
+* Small host-side data (PCM clips, durations, arrival times, token ids) comes
+  from numpy's seeded PCG64 generator.
+* Large tensors (model parameters, synthetic encoder outputs, pre-filled
+  self-attention caches) come from a counter-based integer hash so the very
+  same values can be produced on the CPU (for the oracle) and directly in
+  device memory (for the benchmark at full size) without a multi-gigabyte
+  host round trip.  The hash is Chris Wellons' "lowbias32" integer mixer
+  (published with his hash-prospector project); every value it yields is an
+  integer multiple of a power of two with at most 8 significant bits, so it
+  is exactly representable in float32 *and* bfloat16.  That makes the
+  bf16-path inputs identical on both sides with no rounding step.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+SAMPLE_RATE = 16000
+N_SAMPLES_30S = 480000          # 30 s at 16 kHz: one encoder segment (Section 3.1)
+N_AUDIO_CTX = 1500              # encoder positions per 30-s segment
+N_TEXT_CTX = 448                # maximum output tokens (Section 4.1, setup)
+
+_M32 = 0xFFFFFFFF
+
+
+# ----------------------------------------------------------------------------
+# Model shapes (Whisper family sizes; weights are random, never trained)
+# ----------------------------------------------------------------------------
+@dataclass(frozen=True)
+class ModelShape:
+    name: str
+    n_mels: int
+    d_model: int
+    n_enc: int
+    n_dec: int
+    n_head: int
+    d_ffn: int
+    vocab: int
+    dtype: str                  # "f32" or "bf16": storage type of matrices/activations
+
+    @property
+    def d_head(self) -> int:
+        return self.d_model // self.n_head
+
+
+SHAPES = {
+    "tiny": ModelShape("tiny", 80, 384, 4, 4, 6, 1536, 51865, "f32"),
+    "base": ModelShape("base", 80, 512, 6, 6, 8, 2048, 51865, "bf16"),
+    "small": ModelShape("small", 80, 768, 12, 12, 12, 3072, 51865, "bf16"),
+    "large-v3": ModelShape("large-v3", 128, 1280, 32, 32, 20, 5120, 51866, "bf16"),
+}
+
+
+def reduced_shape(shape: ModelShape, n_enc: int, n_dec: int, vocab: int | None = None,
+                  dtype: str | None = None) -> ModelShape:
+    """Same widths, fewer layers / smaller vocabulary: for fast parity cases."""
+    return ModelShape(shape.name + f"-l{n_enc}x{n_dec}", shape.n_mels, shape.d_model, n_enc,
+                      n_dec, shape.n_head, shape.d_ffn, vocab or shape.vocab,
+                      dtype or shape.dtype)
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    shape: str
+    seed: int
+    batch: int
+    note: str
+    extra: dict = field(default_factory=dict)
+
+
+# The five measured workloads.  Seeds are 20260311 + index.
+WORKLOADS = {
+    "tiny-fp32": Workload("tiny-fp32", "tiny", 20260311, 1,
+                          "one 4-s clip, 16 teacher-forced steps", {"clip_s": 4.0, "steps": 16}),
+    "base-bf16": Workload("base-bf16", "base", 20260312, 8,
+                          "lognormal durations (median 6 s, sigma 0.6) clipped to [1,30] s"),
+    "small-bf16-hrrn": Workload("small-bf16-hrrn", "small", 20260313, 32,
+                                "256 Poisson requests (20/s), durations U[1,30] s, HRRN batches of 32",
+                                {"n_requests": 256, "rate": 20.0}),
+    "large-v3-encoder": Workload("large-v3-encoder", "large-v3", 20260314, 64,
+                                 "64 full 30-s clips through the encoder"),
+    "large-v3-decode": Workload("large-v3-decode", "large-v3", 20260315, 128,
+                                "128 sequences, self-KV lengths U[10,400], 1500 cross positions",
+                                {"n_requests": 2000, "kv_lo": 10, "kv_hi": 400}),
+}
+
+
+# ----------------------------------------------------------------------------
+# Counter-based hash generator (bit-identical on CPU and GPU)
+# ----------------------------------------------------------------------------
+def lowbias32_py(x: int) -> int:
+    """Chris Wellons' lowbias32 mixer on a Python int (reference definition)."""
+    x &= _M32
+    x ^= x >> 16
+    x = (x * 0x7FEB352D) & _M32
+    x ^= x >> 15
+    x = (x * 0x846CA68B) & _M32
+    x ^= x >> 16
+    return x
+
+
+def stream_keys(seed: int, stream: int) -> tuple[int, int]:
+    k1 = lowbias32_py((seed & _M32) ^ lowbias32_py(stream & _M32))
+    k2 = lowbias32_py(k1 ^ 0x5BD1E995)
+    return k1, k2
+
+
+def hash_py(seed: int, stream: int, idx: int) -> int:
+    k1, k2 = stream_keys(seed, stream)
+    return lowbias32_py((lowbias32_py(idx ^ k1) + k2) & _M32)
+
+
+def _mul32_t(x, c: int):
+    # (x * c) mod 2^32 for int64 tensors holding values < 2^32, with no
+    # intermediate above 2^49 (so no signed overflow anywhere).
+    lo, hi = c & 0xFFFF, c >> 16
+    return (x * lo + (((x * hi) & 0xFFFF) << 16)) & _M32
+
+
+def _lowbias32_t(x):
+    x = x ^ (x >> 16)
+    x = _mul32_t(x, 0x7FEB352D)
+    x = x ^ (x >> 15)
+    x = _mul32_t(x, 0x846CA68B)
+    x = x ^ (x >> 16)
+    return x
+
+
+def hash_tensor(seed: int, stream: int, start: int, count: int, device="cpu"):
+    """uint32 hash values (in int64) for counters start .. start+count-1."""
+    import torch
+    k1, k2 = stream_keys(seed, stream)
+    idx = torch.arange(start, start + count, dtype=torch.int64, device=device)
+    h = _lowbias32_t(idx ^ k1)
+    return _lowbias32_t((h + k2) & _M32)
+
+
+def grid_values(seed: int, stream: int, shape, kmax: int, bits: int, device="cpu",
+                offset: float = 0.0, chunk: int = 1 << 24):
+    """float32 tensor of (k * 2^-bits + offset), k uniform on [-kmax, kmax].
+
+    kmax <= 255 keeps every k*2^-bits exactly representable in bfloat16; with
+    offset 1.0 (LayerNorm gains) the value is still exact in float32.
+    """
+    import torch
+    assert 0 < kmax <= 255
+    numel = int(np.prod(shape)) if len(shape) else 1
+    out = torch.empty(numel, dtype=torch.float32, device=device)
+    levels = 2 * kmax + 1
+    scale = 2.0 ** (-bits)
+    for s in range(0, numel, chunk):
+        n = min(chunk, numel - s)
+        h = hash_tensor(seed, stream, s, n, device)
+        k = ((h * levels) >> 32) - kmax
+        v = k.to(torch.float32) * scale
+        if offset:
+            v = v + offset
+        out[s:s + n] = v
+    return out.view(*shape)
+
+
+# ----------------------------------------------------------------------------
+# Model parameters
+# ----------------------------------------------------------------------------
+def param_specs(shape: ModelShape):
+    """Ordered (name, shape, kind) for every parameter tensor.
+
+    kind: "w" matrix/bias ~ std 0.02, "g" LayerNorm gain 1 + small, "b"
+    LayerNorm shift.  The order is the load order of the C ABI.
+    """
+    d, f, m = shape.d_model, shape.d_ffn, shape.n_mels
+    specs = []
+    if shape.n_enc > 0:
+        specs += [("conv1.w", (d, m, 3), "w"), ("conv1.b", (d,), "w"),
+                  ("conv2.w", (d, d, 3), "w"), ("conv2.b", (d,), "w")]
+        for l in range(shape.n_enc):
+            p = f"enc.{l}."
+            specs += [(p + "attn_ln.g", (d,), "g"), (p + "attn_ln.b", (d,), "b"),
+                      (p + "q.w", (d, d), "w"), (p + "q.b", (d,), "w"),
+                      (p + "k.w", (d, d), "w"),
+                      (p + "v.w", (d, d), "w"), (p + "v.b", (d,), "w"),
+                      (p + "o.w", (d, d), "w"), (p + "o.b", (d,), "w"),
+                      (p + "mlp_ln.g", (d,), "g"), (p + "mlp_ln.b", (d,), "b"),
+                      (p + "fc1.w", (f, d), "w"), (p + "fc1.b", (f,), "w"),
+                      (p + "fc2.w", (d, f), "w"), (p + "fc2.b", (d,), "w")]
+        specs += [("ln_post.g", (d,), "g"), ("ln_post.b", (d,), "b")]
+    if shape.n_dec > 0:
+        specs += [("tok_emb", (shape.vocab, d), "w"), ("pos_emb", (N_TEXT_CTX, d), "w")]
+        for l in range(shape.n_dec):
+            p = f"dec.{l}."
+            specs += [(p + "attn_ln.g", (d,), "g"), (p + "attn_ln.b", (d,), "b"),
+                      (p + "q.w", (d, d), "w"), (p + "q.b", (d,), "w"),
+                      (p + "k.w", (d, d), "w"),
+                      (p + "v.w", (d, d), "w"), (p + "v.b", (d,), "w"),
+                      (p + "o.w", (d, d), "w"), (p + "o.b", (d,), "w"),
+                      (p + "xattn_ln.g", (d,), "g"), (p + "xattn_ln.b", (d,), "b"),
+                      (p + "xq.w", (d, d), "w"), (p + "xq.b", (d,), "w"),
+                      (p + "xk.w", (d, d), "w"),
+                      (p + "xv.w", (d, d), "w"), (p + "xv.b", (d,), "w"),
+                      (p + "xo.w", (d, d), "w"), (p + "xo.b", (d,), "w"),
+                      (p + "mlp_ln.g", (d,), "g"), (p + "mlp_ln.b", (d,), "b"),
+                      (p + "fc1.w", (f, d), "w"), (p + "fc1.b", (f,), "w"),
+                      (p + "fc2.w", (d, f), "w"), (p + "fc2.b", (d,), "w")]
+        specs += [("ln.g", (d,), "g"), ("ln.b", (d,), "b")]
+    return specs
+
+
+def model_params(shape: ModelShape, seed: int, device="cpu"):
+    """Ordered dict name -> float32 tensor (values exact in bfloat16 for matrices)."""
+    params = {}
+    for i, (name, shp, kind) in enumerate(param_specs(shape)):
+        if kind == "g":
+            params[name] = grid_values(seed, i, shp, 141, 12, device, offset=1.0)
+        else:
+            params[name] = grid_values(seed, i, shp, 141, 12, device)
+    return params
+
+
+def encoder_output(seed: int, index: int, d_model: int, device="cpu"):
+    """Synthetic encoder output E [1500][d], std ~1, bf16-exact (stream 10^6 + index)."""
+    return grid_values(seed, 1_000_000 + index, (N_AUDIO_CTX, d_model), 221, 7, device)
+
+
+def self_kv_prefix(seed: int, index: int, n_layers: int, n_head: int, length: int,
+                   d_head: int = 64, device="cpu"):
+    """Synthetic pre-filled self-attention cache [L][2][H][length][64], std ~0.7."""
+    return grid_values(seed, 2_000_000 + index, (n_layers, 2, n_head, length, d_head), 155, 7,
+                       device)
+
+
+# ----------------------------------------------------------------------------
+# Host-side workload data
+# ----------------------------------------------------------------------------
+def pcm_clip(seed: int, index: int, n_samples: int) -> np.ndarray:
+    """Sum of 3 sines plus N(0, 0.05) noise, float32, `n_samples` long.
+
+    f ~ U[100, 4000] Hz, amplitude ~ U[0.1, 0.3], phase ~ U[0, 2 pi).
+    """
+    rng = np.random.default_rng([seed, 7, index])
+    f = rng.uniform(100.0, 4000.0, 3)
+    a = rng.uniform(0.1, 0.3, 3)
+    ph = rng.uniform(0.0, 2.0 * np.pi, 3)
+    t = np.arange(n_samples, dtype=np.float64) / SAMPLE_RATE
+    x = np.zeros(n_samples, dtype=np.float64)
+    for i in range(3):
+        x += a[i] * np.sin(2.0 * np.pi * f[i] * t + ph[i])
+    x += rng.normal(0.0, 0.05, n_samples)
+    return x.astype(np.float32)
+
+
+def durations_lognormal(seed: int, n: int, median_s: float = 6.0, sigma: float = 0.6,
+                        lo: float = 1.0, hi: float = 30.0) -> np.ndarray:
+    """Right-skewed durations standing in for LibriSpeech test-clean (Section 4.1)."""
+    rng = np.random.default_rng([seed, 11])
+    d = np.exp(math.log(median_s) + sigma * rng.standard_normal(n))
+    return np.clip(d, lo, hi)
+
+
+def durations_uniform(seed: int, n: int, lo: float = 1.0, hi: float = 30.0) -> np.ndarray:
+    """Flat durations standing in for the synthetic split (Section 4.1)."""
+    rng = np.random.default_rng([seed, 13])
+    return rng.uniform(lo, hi, n)
+
+
+def n_samples_of(durations_s) -> np.ndarray:
+    return np.rint(np.asarray(durations_s) * SAMPLE_RATE).astype(np.int64)
+
+
+def poisson_arrivals_us(seed: int, n: int, rate_per_s: float) -> np.ndarray:
+    """Poisson arrival times (burstiness 1.0) in integer microseconds."""
+    rng = np.random.default_rng([seed, 17])
+    gaps = rng.exponential(1.0 / rate_per_s, n)
+    return np.rint(np.cumsum(gaps) * 1e6).astype(np.int64)
+
+
+def token_ids(seed: int, shape, vocab: int) -> np.ndarray:
+    rng = np.random.default_rng([seed, 19])
+    return rng.integers(0, vocab, size=shape, dtype=np.int64).astype(np.int32)
+
+
+def kv_lengths(seed: int, n: int, lo: int = 10, hi: int = 400) -> np.ndarray:
+    rng = np.random.default_rng([seed, 23])
+    return rng.integers(lo, hi + 1, size=n, dtype=np.int64).astype(np.int32)

@@ -1,0 +1,44 @@
+"""The seeded generators: the tensor hash equals its scalar definition, and
+generated values are exact in bfloat16."""
+import numpy as np
+import torch
+
+from paper_2603_11273_amd import synth
+
+
+def test_lowbias32_known_value_and_tensor_route():
+    # the mixer is a bijection on 32 bits; 0 maps to 0
+    assert synth.lowbias32_py(0) == 0
+    idx = list(range(0, 5000, 7)) + [2**32 - 1, 2**31, 123456789]
+    h = synth.hash_tensor(20260311, 5, 0, 5000)
+    for i in idx[:-3]:
+        assert int(h[i]) == synth.hash_py(20260311, 5, i)
+    big = synth.hash_tensor(3, 1, 2**32 - 3, 3)
+    assert [int(x) for x in big] == [synth.hash_py(3, 1, i) for i in range(2**32 - 3, 2**32)]
+
+
+def test_grid_values_exact_in_bf16():
+    v = synth.grid_values(1, 2, (4096,), 141, 12)
+    assert torch.equal(v, v.to(torch.bfloat16).to(torch.float32))
+    assert abs(float(v.std()) - 0.02) < 0.002
+    g = synth.grid_values(1, 3, (4096,), 141, 12, offset=1.0)
+    assert torch.equal(g - 1.0, (g - 1.0).to(torch.bfloat16).to(torch.float32))
+    e = synth.encoder_output(5, 0, 64)
+    assert torch.equal(e, e.to(torch.bfloat16).to(torch.float32))
+    assert abs(float(e.std()) - 1.0) < 0.05
+
+
+def test_chunking_does_not_change_values():
+    a = synth.grid_values(7, 1, (1000,), 100, 8, chunk=1 << 24)
+    b = synth.grid_values(7, 1, (1000,), 100, 8, chunk=97)
+    assert torch.equal(a, b)
+
+
+def test_workload_distributions():
+    d = synth.durations_lognormal(1, 20000)
+    assert 1.0 <= d.min() and d.max() <= 30.0
+    assert 6.5 < d.mean() < 7.8 and np.median(d) < d.mean()       # right-skewed
+    u = synth.durations_uniform(1, 20000)
+    assert abs(u.mean() - 15.5) < 0.3
+    a = synth.poisson_arrivals_us(1, 5000, 20.0)
+    assert np.all(np.diff(a) >= 0) and abs(a[-1] / 1e6 / 5000 - 0.05) < 0.005
