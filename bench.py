@@ -1,0 +1,253 @@
+"""Benchmark of one engine step of the large-v3-shaped ASR path on one MI355X.
+
+A step is one pass of the whole hot path on one batch of synthetic input:
+
+  * submit 64 requests of 30 s of seeded PCM (resident in HBM) and pop them
+    from the duration-aware queue (SJF on duration, Section 3.2);
+  * prefill them: log-mel front-end, conv stem, 32 encoder layers, ln_post,
+    cross K/V of all 32 decoder layers into 64 fresh slots;
+  * one teacher-forced decode step of 128 running sequences (self-attention
+    caches pre-filled to lengths U[10, 400], 1500 cross positions each), with
+    the vocabulary projection fused with argmax;
+  * slot bookkeeping (the 64 prefill slots are released for the next step).
+
+The 128 running sequences come from an SJF-ordered stream of 2000 requests
+with lognormal durations.  Weights are random (seeded); no dataset is read.
+
+Prints ONE JSON line.  `value` is audio-seconds of speech prefilled per
+second of wall time over whole steps (the decode step riding along);
+`decode_tokens_per_s` and `encoder_audio_s_per_s` use the phase times
+measured with HIP events inside the same timed steps.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--prefill", type=int, default=64)
+    ap.add_argument("--decode", type=int, default=128)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=25.0)
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
+                          "(the path shards by request, see DESIGN.md)"}))
+        sys.exit(2)
+    if int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print(json.dumps({"error": "one GPU only"}))
+        sys.exit(2)
+    import torch
+    from paper_2603_11273_amd import asr, synth
+
+    if args.warmup + args.steps > 45:
+        raise SystemExit("warmup + steps must stay <= 45 (decode positions stay below 448)")
+    P, D = args.prefill, args.decode
+    shape = synth.SHAPES["large-v3"]
+    enc_wl = synth.WORKLOADS["large-v3-encoder"]
+    dec_wl = synth.WORKLOADS["large-v3-decode"]
+    dev = torch.device("cuda:0")
+
+    # ---------------------------------------------------------------- context
+    cfg = asr.model_cfg(shape, max_slots=D + P, max_prefill=P, max_decode=D, max_queue=4096)
+    ctx = asr.Context(cfg, device=0)
+    log(f"workspace {ctx.workspace_size() / 2**30:.1f} GiB")
+    ctx.bind()
+    t0 = time.time()
+    params = synth.model_params(shape, enc_wl.seed, device=dev)
+    ctx.load_weights(list(params.values()), on_device=True)
+    torch.cuda.synchronize()
+    log(f"weights generated + loaded in {time.time() - t0:.1f} s")
+
+    # ------------------------------------------- the running decode sequences
+    # SJF-ordered stream of 2000 lognormal requests (queue-only context)
+    q = asr.Context(cfg, device=-1)
+    q.set_policy(asr.SJF)
+    n_req = dec_wl.extra["n_requests"]
+    durs = synth.durations_lognormal(dec_wl.seed, n_req)
+    ns = synth.n_samples_of(durs)
+    arr = synth.poisson_arrivals_us(dec_wl.seed, n_req, 25.0)
+    tq = time.perf_counter()
+    for i in range(n_req):
+        q.submit(i, None, n_samples=int(ns[i]), duration_us=int(ns[i]) * 10**6 // 16000,
+                 arrival_us=int(arr[i]))
+    running = q.pop_batch(int(arr[n_req // 2]), D)
+    queue_us_per_req = (time.perf_counter() - tq) * 1e6 / n_req
+    steps_left = [max(1, min(448, (27 * int(ns[i]) + 80000) // 160000)) for i in running]
+
+    kv_len = synth.kv_lengths(dec_wl.seed, D, dec_wl.extra["kv_lo"], dec_wl.extra["kv_hi"])
+    t0 = time.time()
+    for s0 in range(0, D, P):
+        idx = list(range(s0, min(D, s0 + P)))
+        E = torch.stack([synth.encoder_output(dec_wl.seed, b, shape.d_model, device=dev)
+                         for b in idx])
+        ctx.debug_set_encoder_out(idx, [-1] * len(idx), [steps_left[b] for b in idx], E,
+                                  on_device=True)
+        del E
+    for b in range(D):
+        kv = synth.self_kv_prefix(dec_wl.seed, b, shape.n_dec, shape.n_head, device=dev)
+        ctx.debug_set_self_kv(b, kv, int(kv_len[b]), on_device=True)
+        del kv
+    torch.cuda.synchronize()
+    log(f"{D} decode slots filled in {time.time() - t0:.1f} s")
+
+    # -------------------------------------------------- prefill audio in HBM
+    pcm_host = np.stack([synth.pcm_clip(enc_wl.seed, i, synth.N_SAMPLES_30S) for i in range(P)])
+    pcm = torch.from_numpy(pcm_host).to(dev)
+    toks = synth.token_ids(dec_wl.seed, (args.warmup + args.steps, D), shape.vocab)
+    del params
+    torch.cuda.empty_cache()
+
+    next_id = [10**6]
+    vclock = [int(arr[-1]) + 1]
+
+    def one_step(k):
+        ids = []
+        for i in range(P):
+            ctx.submit(next_id[0], pcm[i], n_samples=synth.N_SAMPLES_30S,
+                       arrival_us=vclock[0] + i, on_device=True)
+            next_id[0] += 1
+        popped = ctx.pop_batch(vclock[0] + P, P)
+        vclock[0] += 10**6
+        out = ctx.step(prefill_ids=popped, slots=list(range(D)), tokens=[int(t) for t in toks[k]])
+        for s in out["slot_of"]:
+            ctx.release_slot(int(s))
+        return out
+
+    ctx.set_policy(asr.SJF)
+    for k in range(args.warmup):
+        one_step(k)
+    torch.cuda.synchronize()
+    log("warmup done")
+
+    ctx.reset_timing()
+    ctx.set_timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        one_step(args.warmup + k)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ctx.set_timing(False)
+    tm = ctx.timing()
+    log(f"timed {args.steps} steps in {wall:.3f} s")
+
+    ms_step = wall * 1e3 / args.steps
+    audio_s = P * 30.0
+    enc_ms = tm["prefill"]["ms"] / args.steps
+    dec_ms = tm["decode"]["ms"] / args.steps
+    g = tm["gemm"]
+    gemm_tflops = g["flops"] / (g["ms"] * 1e-3) / 1e12 if g["ms"] else 0.0
+    da = tm["dattn"]
+    dattn_gbs = da["bytes"] / (da["ms"] * 1e-3) / 1e9 if da["ms"] else 0.0
+    enc_flops = tm["gemm"]["flops"] + tm["attn"]["flops"]
+    dec_bytes = tm["dgemm"]["bytes"] + tm["dattn"]["bytes"] + tm["vocab"]["bytes"]
+    kernels = {k: {"ms_per_step": v["ms"] / args.steps, "launches_per_step": v["launches"] / args.steps}
+               for k, v in tm.items()}
+
+    result = {
+        "metric": "encoder audio-sec/s + decode tokens/s at large-v3 shape; % MFMA peak / % HBM BW",
+        "value": round(audio_s / (ms_step * 1e-3), 1),
+        "unit": "audio-s/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded PCM, random-init weights; no dataset)",
+        "config": {"workload": f"large-v3 step: prefill {P} x 30 s clips + decode {D} sequences "
+                               "(self-KV U[10,400], 1500 cross positions)",
+                   "prefill_clips": P, "decode_rows": D, "n_mels": 128, "d_model": 1280,
+                   "layers": "32+32", "vocab": 51866, "parallelism": "none (1 GPU)"},
+        "encoder_audio_s_per_s": round(audio_s / (enc_ms * 1e-3), 1) if enc_ms else None,
+        "decode_tokens_per_s": round(D / (dec_ms * 1e-3), 1) if dec_ms else None,
+        "prefill_ms": round(enc_ms, 3),
+        "decode_ms": round(dec_ms, 3),
+        "encoder_mfma_frac": round(enc_flops / (enc_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)
+        if enc_ms else None,
+        "decode_hbm_frac": round(dec_bytes / (dec_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)
+        if dec_ms else None,
+        "queue_us_per_request": round(queue_us_per_req, 3),
+        "kernels": kernels,
+        "roofline": {"bound": "mfma", "kernel": "gemm_bf16 (encoder, stem, cross K/V)",
+                     "achieved": round(gemm_tflops, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None},
+        "roofline_decode": {"bound": "hbm", "kernel": "decode attention (self + cross)",
+                            "achieved": round(dattn_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                            "frac": round(dattn_gbs / PEAK_HBM_GBS, 4), "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(shape, enc_wl, dec_wl, pcm_host[0], P, D,
+                                              ms_step, args.cpu_budget_s)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(shape, enc_wl, dec_wl, pcm0, P, D, ms_step, budget_s):
+    """The oracle, as it stands, on a bounded sample of the same step: one clip
+    through mel + encoder + cross K/V and one sequence through one decode step,
+    extrapolated linearly to the P clips and D sequences of a step."""
+    import torch
+    from oracle import mel as OM
+    from oracle import whisper as OW
+    from paper_2603_11273_amd import synth
+    cores = len(os.sched_getaffinity(0))
+    torch.set_num_threads(cores)
+    log(f"cpu baseline on {cores} cores")
+    # parameters from the same generator (device copy brought to the host)
+    params = {k: v.cpu() for k, v in synth.model_params(shape, enc_wl.seed, device="cuda").items()}
+    t0 = time.perf_counter()
+    mel = OM.log_mel(pcm0, shape.n_mels)
+    E = OW.encode(mel, params, shape.n_enc, shape.n_head)
+    ckv = OW.cross_kv(E, params, shape.n_dec)
+    t_clip = time.perf_counter() - t0
+    log(f"oracle: one clip prefill {t_clip:.1f} s")
+    kv = synth.self_kv_prefix(dec_wl.seed, 0, shape.n_dec, shape.n_head).numpy().astype(np.float64)
+    L = 205
+    kp = [kv[l, 0, :, :L].transpose(1, 0, 2).reshape(L, -1) for l in range(shape.n_dec)]
+    vp = [kv[l, 1, :, :L].transpose(1, 0, 2).reshape(L, -1) for l in range(shape.n_dec)]
+    st = OW.DecoderState(shape.n_dec, shape.d_model, kp, vp)
+    t0 = time.perf_counter()
+    OW.decoder_step(1, st, ckv, params, shape.n_dec, shape.n_head)
+    t_tok = time.perf_counter() - t0
+    log(f"oracle: one sequence decode step {t_tok:.1f} s")
+    step_s = P * t_clip + D * t_tok
+    return {"value": round(P * 30.0 / step_s, 4), "unit": "audio-s/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"1 clip (30 s) mel+encoder+cross-K/V ({t_clip:.1f} s) and 1 sequence "
+                      f"decode step at self-KV length 205 ({t_tok:.2f} s), fp64 numpy, "
+                      f"extrapolated to {P} clips + {D} sequences per step",
+            "extrapolated": True,
+            "decode_tokens_per_s": round(1.0 / t_tok, 3),
+            "encoder_audio_s_per_s": round(30.0 / t_clip, 3)}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,481 @@
+// GEMMs of the step.
+//
+//  * gemm_bf16: C = A . W^T on gfx950 MFMA (v_mfma_f32_32x32x16_bf16), bf16
+//    operands, fp32 accumulation, LDS double buffering, fused epilogues
+//    (bias, exact GELU, fp32 residual add, conv-stem row mapping, scatter of
+//    all decoder layers' cross K/V into a slot's cache).
+//  * gemm_f32: the same contract in plain fp32 FMA (the fp32 model path).
+//  * dgemm_bf16 / dgemm_f32: skinny products for the decode rows with K split
+//    across workgroups (weights streamed once), then a reduce kernel that
+//    applies the epilogue.
+//  * vocab_argmax_bf16: the tied vocabulary projection fused with a per-row
+//    argmax (lowest index on ties) over each 64-column tile, finished by a
+//    deterministic cross-tile reduction.
+#include "asr_device.h"
+
+namespace asr {
+
+// ---------------------------------------------------------------------------
+// Epilogue
+// ---------------------------------------------------------------------------
+template <int KIND, typename T>
+__device__ __forceinline__ void epi_apply(const Epilogue& e, int r, int n, float acc) {
+  float v = acc + (e.bias ? e.bias[n] : 0.0f);
+  if constexpr (KIND == EPI_STORE) {
+    St<T>::st((T*)e.out, (int64_t)r * e.ldc + n, v);
+  } else if constexpr (KIND == EPI_GELU) {
+    St<T>::st((T*)e.out, (int64_t)r * e.ldc + n, gelu_erf(v));
+  } else if constexpr (KIND == EPI_RESID) {
+    float* x = (float*)e.out + (int64_t)r * e.ldc + n;
+    *x = *x + v;
+  } else if constexpr (KIND == EPI_CONV1) {
+    int g = r / kFrames, t = r - g * kFrames;
+    int64_t base = (int64_t)g * (kFrames + 1) * e.d_model;
+    St<T>::st((T*)e.out, base + (int64_t)(t + 1) * e.d_model + n, gelu_erf(v));
+    if (t == 0) St<T>::st((T*)e.out, base + n, 0.0f);        // position -1 of conv2
+  } else if constexpr (KIND == EPI_CONV2) {
+    int t = r % kCtx;
+    ((float*)e.out)[(int64_t)r * e.ldc + n] = gelu_erf(v) + e.pos[(int64_t)t * e.ldc + n];
+  } else if constexpr (KIND == EPI_XKV) {
+    int g = r / kCtx, t = r - g * kCtx;
+    int two_d = 2 * e.d_model;
+    int l = n / two_d;
+    int rem = n - l * two_d;
+    int kv = rem >= e.d_model;
+    int hd = rem - kv * e.d_model;
+    int h = hd >> 6, c = hd & 63;
+    int64_t addr = (int64_t)e.slots[g] * e.slot_stride +
+                   ((((int64_t)l * 2 + kv) * e.n_head + h) * kCtx + t) * kHeadDim + c;
+    St<T>::st((T*)e.out, addr, v);
+  }
+}
+
+__device__ __forceinline__ int64_t arow_offset(const AView& a, int r) {
+  int g = r / a.rows_per_batch;
+  return (int64_t)g * a.batch_stride + (int64_t)(r - g * a.rows_per_batch) * a.lda;
+}
+
+// ---------------------------------------------------------------------------
+// bf16 MFMA GEMM
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int WM, int WN, int KIND>
+__global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(AView a, const bf16_t* __restrict__ w,
+                                                          int M, int N, int K, Epilogue e,
+                                                          int n_tn) {
+  constexpr int NT = WM * WN * 64;
+  constexpr int BK = 64;
+  constexpr int LD = BK + 8;                       // padded LDS row (elements)
+  constexpr int TM = BM / WM, TN = BN / WN;
+  constexpr int FM = TM / 32, FN = TN / 32;
+  constexpr int CA = BM * 8 / NT, CB = BN * 8 / NT;
+  static_assert(CA * NT == BM * 8 && CB * NT == BN * 8, "tile/threads");
+  __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * LD];
+  __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BN * LD];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % WM, wn = wave / WM;
+  const int tn = blockIdx.x % n_tn, tm = blockIdx.x / n_tn;
+  const int m0 = tm * BM, n0 = tn * BN;
+
+  const bf16_t* aptr[CA];
+  bool aok[CA];
+  int arow[CA], akc[CA];
+#pragma unroll
+  for (int i = 0; i < CA; ++i) {
+    int c = tid + i * NT;
+    arow[i] = c >> 3;
+    akc[i] = (c & 7) * 8;
+    int r = m0 + arow[i];
+    aok[i] = r < M;
+    aptr[i] = (const bf16_t*)a.ptr + arow_offset(a, aok[i] ? r : 0) + akc[i];
+  }
+  const bf16_t* bptr[CB];
+  bool bok[CB];
+  int brow[CB], bkc[CB];
+#pragma unroll
+  for (int i = 0; i < CB; ++i) {
+    int c = tid + i * NT;
+    brow[i] = c >> 3;
+    bkc[i] = (c & 7) * 8;
+    int n = n0 + brow[i];
+    bok[i] = n < N;
+    bptr[i] = w + (int64_t)(bok[i] ? n : 0) * K + bkc[i];
+  }
+
+  uint4 ra[CA], rb[CB];
+  const uint4 z = {0u, 0u, 0u, 0u};
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < CA; ++i)
+      ra[i] = (aok[i] && k0 + akc[i] < K) ? *(const uint4*)(aptr[i] + k0) : z;
+#pragma unroll
+    for (int i = 0; i < CB; ++i)
+      rb[i] = (bok[i] && k0 + bkc[i] < K) ? *(const uint4*)(bptr[i] + k0) : z;
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < CA; ++i) *(uint4*)&As[buf][arow[i] * LD + akc[i]] = ra[i];
+#pragma unroll
+    for (int i = 0; i < CB; ++i) *(uint4*)&Bs[buf][brow[i] * LD + bkc[i]] = rb[i];
+  };
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int nk = (K + BK - 1) / BK;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  const int lrow = lane & 31, lk = (lane >> 5) * 8;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) gload((kt + 1) * BK);
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      bf16x8 af[FM], bfr[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        af[i] = *(const bf16x8*)&As[cur][(wm * TM + i * 32 + lrow) * LD + kk * 16 + lk];
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        bfr[j] = *(const bf16x8*)&Bs[cur][(wn * TN + j * 32 + lrow) * LD + kk * 16 + lk];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < nk) sstore(cur ^ 1);
+    __syncthreads();
+  }
+
+  // C layout of a 32x32 block: lane holds column lane%32 and, for register r,
+  // row 8*(r/4) + 4*(lane/32) + r%4.
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        int row = m0 + wm * TM + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        int col = n0 + wn * TN + j * 32 + lrow;
+        if (row < M && col < N) epi_apply<KIND, bf16_t>(e, row, col, acc[i][j][r]);
+      }
+}
+
+template <int KIND>
+static void launch_gemm_bf16(const AView& a, const bf16_t* w, int M, int N, int K,
+                             const Epilogue& e, hipStream_t s) {
+  constexpr int BM = 128, BN = 128;
+  int n_tm = (M + BM - 1) / BM, n_tn = (N + BN - 1) / BN;
+  k_gemm_bf16<BM, BN, 2, 2, KIND><<<n_tm * n_tn, 256, 0, s>>>(a, w, M, N, K, e, n_tn);
+}
+
+void gemm_bf16(const AView& a, const bf16_t* w, int M, int N, int K, const Epilogue& e,
+               hipStream_t s) {
+  if (M <= 0 || N <= 0) return;
+  switch (e.kind) {
+    case EPI_STORE: launch_gemm_bf16<EPI_STORE>(a, w, M, N, K, e, s); break;
+    case EPI_GELU: launch_gemm_bf16<EPI_GELU>(a, w, M, N, K, e, s); break;
+    case EPI_RESID: launch_gemm_bf16<EPI_RESID>(a, w, M, N, K, e, s); break;
+    case EPI_CONV1: launch_gemm_bf16<EPI_CONV1>(a, w, M, N, K, e, s); break;
+    case EPI_CONV2: launch_gemm_bf16<EPI_CONV2>(a, w, M, N, K, e, s); break;
+    case EPI_XKV: launch_gemm_bf16<EPI_XKV>(a, w, M, N, K, e, s); break;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// fp32 GEMM (SIMT): 64x64 tile, 256 threads, 4x4 outputs per thread.
+// ---------------------------------------------------------------------------
+template <int KIND>
+__global__ __launch_bounds__(256) void k_gemm_f32(AView a, const float* __restrict__ w, int M,
+                                                  int N, int K, Epilogue e, int n_tn) {
+  constexpr int BM = 64, BN = 64, BK = 16;
+  __shared__ float As[BK][BM + 4];
+  __shared__ float Bs[BK][BN + 4];
+  const int tid = threadIdx.x;
+  const int tn = blockIdx.x % n_tn, tm = blockIdx.x / n_tn;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int lr = tid >> 2, lk = (tid & 3) * 4;      // loader: row, k offset
+  const int ar = m0 + lr, bn = n0 + lr;
+  const float* ap = (const float*)a.ptr + arow_offset(a, ar < M ? ar : 0) + lk;
+  const float* bp = w + (int64_t)(bn < N ? bn : 0) * K + lk;
+  const int ty = tid >> 4, tx = tid & 15;
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < K; k0 += BK) {
+    float4 va = make_float4(0.f, 0.f, 0.f, 0.f), vb = va;
+    if (ar < M && k0 + lk < K) va = *(const float4*)(ap + k0);
+    if (bn < N && k0 + lk < K) vb = *(const float4*)(bp + k0);
+    As[lk + 0][lr] = va.x; As[lk + 1][lr] = va.y; As[lk + 2][lr] = va.z; As[lk + 3][lr] = va.w;
+    Bs[lk + 0][lr] = vb.x; Bs[lk + 1][lr] = vb.y; Bs[lk + 2][lr] = vb.z; Bs[lk + 3][lr] = vb.w;
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < BK; ++k) {
+      float av[4], bv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) av[i] = As[k][ty * 4 + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bv[j] = Bs[k][tx * 4 + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      int row = m0 + ty * 4 + i, col = n0 + tx * 4 + j;
+      if (row < M && col < N) epi_apply<KIND, float>(e, row, col, acc[i][j]);
+    }
+}
+
+template <int KIND>
+static void launch_gemm_f32(const AView& a, const float* w, int M, int N, int K,
+                            const Epilogue& e, hipStream_t s) {
+  int n_tm = (M + 63) / 64, n_tn = (N + 63) / 64;
+  k_gemm_f32<KIND><<<n_tm * n_tn, 256, 0, s>>>(a, w, M, N, K, e, n_tn);
+}
+
+void gemm_f32(const AView& a, const float* w, int M, int N, int K, const Epilogue& e,
+              hipStream_t s) {
+  if (M <= 0 || N <= 0) return;
+  switch (e.kind) {
+    case EPI_STORE: launch_gemm_f32<EPI_STORE>(a, w, M, N, K, e, s); break;
+    case EPI_GELU: launch_gemm_f32<EPI_GELU>(a, w, M, N, K, e, s); break;
+    case EPI_RESID: launch_gemm_f32<EPI_RESID>(a, w, M, N, K, e, s); break;
+    case EPI_CONV1: launch_gemm_f32<EPI_CONV1>(a, w, M, N, K, e, s); break;
+    case EPI_CONV2: launch_gemm_f32<EPI_CONV2>(a, w, M, N, K, e, s); break;
+    case EPI_XKV: launch_gemm_f32<EPI_XKV>(a, w, M, N, K, e, s); break;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Decode GEMMs
+// ---------------------------------------------------------------------------
+// One block: 64 output columns x all decode rows (one wave per 32 rows) over
+// one K-split.  The weight rows are the MFMA "A" operand, the activation rows
+// the "B" operand, so each lane ends with one row's values for 16 columns.
+__global__ __launch_bounds__(256) void k_dgemm_bf16(const bf16_t* __restrict__ x,
+                                                    const bf16_t* __restrict__ w, int D, int N,
+                                                    int K, int kc, float* partial) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n0 = blockIdx.x * 64, split = blockIdx.y;
+  const int kb = split * kc, ke = min(K, kb + kc);
+  const int b0 = wave * 32;
+  if (b0 >= D) return;
+  const int brow = b0 + (lane & 31);
+  const int lk = (lane >> 5) * 8;
+  const bf16_t* xp = x + (int64_t)min(brow, D - 1) * K + lk;
+  const bf16_t* wp0 = w + (int64_t)min(n0 + (lane & 31), N - 1) * K + lk;
+  const bf16_t* wp1 = w + (int64_t)min(n0 + 32 + (lane & 31), N - 1) * K + lk;
+  f32x16 acc0, acc1;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc0[r] = acc1[r] = 0.f;
+#pragma unroll 4
+  for (int k = kb; k < ke; k += 16) {
+    bf16x8 xb = *(const bf16x8*)(xp + k);
+    bf16x8 w0 = *(const bf16x8*)(wp0 + k);
+    bf16x8 w1 = *(const bf16x8*)(wp1 + k);
+    acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w0, xb, acc0, 0, 0, 0);
+    acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w1, xb, acc1, 0, 0, 0);
+  }
+  if (brow >= D) return;
+  float* out = partial + ((int64_t)split * D + brow) * N;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    int n = n0 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+    if (n < N) out[n] = acc0[r];
+    if (n + 32 < N) out[n + 32] = acc1[r];
+  }
+}
+
+static int choose_kc(int N, int K, int max_splits) {
+  // aim for >= ~512 workgroups while keeping each split >= 128 deep
+  int n_tiles = (N + 63) / 64;
+  int splits = (512 + n_tiles - 1) / n_tiles;
+  int max_by_depth = K / 128 > 0 ? K / 128 : 1;
+  if (splits > max_by_depth) splits = max_by_depth;
+  if (splits > max_splits) splits = max_splits;
+  if (splits < 1) splits = 1;
+  int kc = (K + splits - 1) / splits;
+  kc = (kc + 15) / 16 * 16;
+  return kc;
+}
+
+int dgemm_bf16(const bf16_t* x, const bf16_t* w, int D, int N, int K, float* partial,
+               int max_splits, hipStream_t s) {
+  int kc = choose_kc(N, K, max_splits);
+  int splits = (K + kc - 1) / kc;
+  dim3 grid((N + 63) / 64, splits);
+  if (D > 0) k_dgemm_bf16<<<grid, 256, 0, s>>>(x, w, D, N, K, kc, partial);
+  return splits;
+}
+
+int dgemm_f32(const float* x, const float* w, int D, int N, int K, float* partial,
+              int max_splits, hipStream_t s) {
+  (void)max_splits;
+  AView a{x, K, 0, 1 << 30};
+  Epilogue e{};
+  e.kind = EPI_STORE;
+  e.out = partial;
+  e.ldc = N;
+  gemm_f32(a, w, D, N, K, e, s);
+  return 1;
+}
+
+template <typename T>
+__global__ void k_dgemm_reduce(const float* partial, int splits, int D, int N,
+                               const float* bias, int mode, void* out) {
+  int64_t n_all = (int64_t)D * N;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n_all;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    int n = (int)(i % N);
+    float v = bias ? bias[n] : 0.f;
+    for (int s = 0; s < splits; ++s) v += partial[(int64_t)s * n_all + i];
+    if (mode == 0) {
+      St<T>::st((T*)out, i, v);
+    } else if (mode == 1) {
+      St<T>::st((T*)out, i, gelu_erf(v));
+    } else {
+      ((float*)out)[i] += v;
+    }
+  }
+}
+template <typename T>
+void dgemm_reduce(const float* partial, int splits, int D, int N, const float* bias, int mode,
+                  void* out, hipStream_t s) {
+  int64_t n = (int64_t)D * N;
+  if (n <= 0) return;
+  int g = (int)((n + 255) / 256);
+  if (g > 8192) g = 8192;
+  k_dgemm_reduce<T><<<g, 256, 0, s>>>(partial, splits, D, N, bias, mode, out);
+}
+template void dgemm_reduce<float>(const float*, int, int, int, const float*, int, void*,
+                                  hipStream_t);
+template void dgemm_reduce<bf16_t>(const float*, int, int, int, const float*, int, void*,
+                                   hipStream_t);
+
+// ---------------------------------------------------------------------------
+// Vocabulary projection + argmax
+// ---------------------------------------------------------------------------
+int vocab_tiles(int V) { return (V + 63) / 64; }
+
+// Larger key = larger value, then lower index.  Any NaN gets the largest
+// value key so that it always wins and the finishing pass reports it.
+__device__ __forceinline__ uint64_t argmax_key(float v, int n) {
+  uint32_t o = (v != v) ? 0xffffffffu : ordered_u32(v);
+  return ((uint64_t)o << 32) | (uint64_t)(0xffffffffu - (uint32_t)n);
+}
+
+__global__ __launch_bounds__(256) void k_vocab_bf16(const bf16_t* __restrict__ x,
+                                                    const bf16_t* __restrict__ emb, int D, int V,
+                                                    int K, uint64_t* keys, int n_tiles,
+                                                    float* logits) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n0 = blockIdx.x * 64;
+  const int b0 = wave * 32;
+  if (b0 >= D) return;
+  const int brow = b0 + (lane & 31);
+  const int lk = (lane >> 5) * 8;
+  const bf16_t* xp = x + (int64_t)min(brow, D - 1) * K + lk;
+  const bf16_t* wp0 = emb + (int64_t)min(n0 + (lane & 31), V - 1) * K + lk;
+  const bf16_t* wp1 = emb + (int64_t)min(n0 + 32 + (lane & 31), V - 1) * K + lk;
+  f32x16 acc0, acc1;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc0[r] = acc1[r] = 0.f;
+#pragma unroll 4
+  for (int k = 0; k < K; k += 16) {
+    bf16x8 xb = *(const bf16x8*)(xp + k);
+    bf16x8 w0 = *(const bf16x8*)(wp0 + k);
+    bf16x8 w1 = *(const bf16x8*)(wp1 + k);
+    acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w0, xb, acc0, 0, 0, 0);
+    acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w1, xb, acc1, 0, 0, 0);
+  }
+  uint64_t best = 0;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    int n = n0 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+    if (n < V) {
+      uint64_t k0 = argmax_key(acc0[r], n);
+      best = k0 > best ? k0 : best;
+      if (logits && brow < D) logits[(int64_t)brow * V + n] = acc0[r];
+    }
+    if (n + 32 < V) {
+      uint64_t k1 = argmax_key(acc1[r], n + 32);
+      best = k1 > best ? k1 : best;
+      if (logits && brow < D) logits[(int64_t)brow * V + n + 32] = acc1[r];
+    }
+  }
+  uint32_t lo = (uint32_t)best, hi = (uint32_t)(best >> 32);
+  uint32_t plo = __shfl_xor(lo, 32, 64), phi = __shfl_xor(hi, 32, 64);
+  uint64_t other = ((uint64_t)phi << 32) | plo;
+  best = other > best ? other : best;
+  if (lane < 32 && brow < D) keys[(int64_t)brow * n_tiles + blockIdx.x] = best;
+}
+
+void vocab_argmax_bf16(const bf16_t* x, const bf16_t* emb, int D, int V, int K, uint64_t* keys,
+                       int n_tiles, float* logits, hipStream_t s) {
+  if (D > 0) k_vocab_bf16<<<n_tiles, 256, 0, s>>>(x, emb, D, V, K, keys, n_tiles, logits);
+}
+
+void vocab_logits_f32(const float* x, const float* emb, int D, int V, int K, float* logits,
+                      hipStream_t s) {
+  AView a{x, K, 0, 1 << 30};
+  Epilogue e{};
+  e.kind = EPI_STORE;
+  e.out = logits;
+  e.ldc = V;
+  gemm_f32(a, emb, D, V, K, e, s);
+}
+
+__global__ void k_logits_keys(const float* logits, int D, int V, uint64_t* keys, int n_tiles) {
+  int tile = blockIdx.x, b = blockIdx.y;
+  int n = tile * 64 + threadIdx.x;
+  uint64_t best = 0;
+  if (n < V) best = argmax_key(logits[(int64_t)b * V + n], n);
+  for (int o = 32; o > 0; o >>= 1) {
+    uint32_t lo = __shfl_xor((uint32_t)best, o, 64), hi = __shfl_xor((uint32_t)(best >> 32), o, 64);
+    uint64_t other = ((uint64_t)hi << 32) | lo;
+    best = other > best ? other : best;
+  }
+  if (threadIdx.x == 0) keys[(int64_t)b * n_tiles + tile] = best;
+}
+void logits_argmax_keys(const float* logits, int D, int V, uint64_t* keys, int n_tiles,
+                        hipStream_t s) {
+  if (D > 0) k_logits_keys<<<dim3(n_tiles, D), 64, 0, s>>>(logits, D, V, keys, n_tiles);
+}
+
+// One wave per row: max key over the row's tiles; NaN winner raises the flag.
+__global__ void k_argmax_finish(const uint64_t* keys, int n_tiles, int32_t* out,
+                                int32_t* nan_flag) {
+  int b = blockIdx.x;
+  uint64_t best = 0;
+  for (int t = threadIdx.x; t < n_tiles; t += 64) {
+    uint64_t k = keys[(int64_t)b * n_tiles + t];
+    best = k > best ? k : best;
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    uint32_t lo = __shfl_xor((uint32_t)best, o, 64), hi = __shfl_xor((uint32_t)(best >> 32), o, 64);
+    uint64_t other = ((uint64_t)hi << 32) | lo;
+    best = other > best ? other : best;
+  }
+  if (threadIdx.x == 0) {
+    float v = from_ordered_u32((uint32_t)(best >> 32));
+    out[b] = (int32_t)(0xffffffffu - (uint32_t)best);
+    if (v != v) atomicOr(nan_flag, 1);
+  }
+}
+void argmax_finish(const uint64_t* keys, int D, int n_tiles, int32_t* out, int32_t* nan_flag,
+                   hipStream_t s) {
+  if (D > 0) k_argmax_finish<<<D, 64, 0, s>>>(keys, n_tiles, out, nan_flag);
+}
+
+}  // namespace asr

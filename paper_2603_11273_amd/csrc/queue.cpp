@@ -1,0 +1,102 @@
+#include "queue.h"
+
+#include <algorithm>
+
+namespace asr {
+
+int64_t WaitQueue::job_of(const QEntry& e) const {
+  if (kd_ == 0) return e.dur_us;
+  if (e.n_samples <= 0) return e.max_tokens;                 // request-level fallback
+  int64_t est = (e.n_samples * (int64_t)kn_) / ((int64_t)e.sample_rate * kd_);
+  return est < 1 ? 1 : est;
+}
+
+// True when a is served before b.
+bool WaitQueue::before(const QEntry& a, const QEntry& b, int64_t now_us) const {
+  if (policy_ == HRRN) {
+    // (w_a + e_a)/e_a > (w_b + e_b)/e_b  <=>  w_a * e_b > w_b * e_a
+    __int128 lhs = (__int128)(now_us - a.arrival_us) * b.job;
+    __int128 rhs = (__int128)(now_us - b.arrival_us) * a.job;
+    if (lhs != rhs) return lhs > rhs;
+  }
+  if (policy_ != FCFS && a.job != b.job) return a.job < b.job;
+  if (a.arrival_us != b.arrival_us) return a.arrival_us < b.arrival_us;
+  return a.id < b.id;
+}
+
+void WaitQueue::rebuild() {
+  for (auto& e : items_) e.job = job_of(e);
+  if (policy_ != HRRN)
+    std::make_heap(items_.begin(), items_.end(),
+                   [this](const QEntry& x, const QEntry& y) { return before(y, x, 0); });
+}
+
+void WaitQueue::set_policy(int policy, int32_t kappa_num, int32_t kappa_den) {
+  policy_ = policy;
+  kn_ = kappa_num;
+  kd_ = kappa_den;
+  rebuild();
+}
+
+void WaitQueue::push(QEntry e) {
+  e.job = job_of(e);
+  ids_.insert(e.id);
+  items_.push_back(e);
+  if (policy_ != HRRN)
+    std::push_heap(items_.begin(), items_.end(),
+                   [this](const QEntry& x, const QEntry& y) { return before(y, x, 0); });
+}
+
+std::vector<int64_t> WaitQueue::rank(int64_t now_us) const {
+  std::vector<const QEntry*> el;
+  el.reserve(items_.size());
+  for (const auto& e : items_)
+    if (e.arrival_us <= now_us) el.push_back(&e);
+  std::sort(el.begin(), el.end(),
+            [&](const QEntry* x, const QEntry* y) { return before(*x, *y, now_us); });
+  std::vector<int64_t> ids;
+  ids.reserve(el.size());
+  for (auto* e : el) ids.push_back(e->id);
+  return ids;
+}
+
+std::vector<QEntry> WaitQueue::pop_batch(int64_t now_us, int max_n) {
+  std::vector<QEntry> out;
+  if (max_n <= 0) return out;
+  if (policy_ == HRRN) {
+    // ratios depend on now: a linear scan per pop
+    while ((int)out.size() < max_n) {
+      int best = -1;
+      for (int i = 0; i < (int)items_.size(); ++i) {
+        if (items_[i].arrival_us > now_us) continue;
+        if (best < 0 || before(items_[i], items_[best], now_us)) best = i;
+      }
+      if (best < 0) break;
+      out.push_back(items_[best]);
+      items_[best] = items_.back();
+      items_.pop_back();
+    }
+  } else {
+    auto cmp = [this](const QEntry& x, const QEntry& y) { return before(y, x, 0); };
+    std::vector<QEntry> later;                 // popped but not yet arrived
+    while ((int)out.size() < max_n && !items_.empty()) {
+      std::pop_heap(items_.begin(), items_.end(), cmp);
+      QEntry e = items_.back();
+      items_.pop_back();
+      if (e.arrival_us <= now_us) {
+        out.push_back(e);
+      } else {
+        later.push_back(e);
+        if (policy_ == FCFS) break;            // arrival order: the rest arrive later still
+      }
+    }
+    for (auto& e : later) {
+      items_.push_back(e);
+      std::push_heap(items_.begin(), items_.end(), cmp);
+    }
+  }
+  for (auto& e : out) ids_.erase(e.id);
+  return out;
+}
+
+}  // namespace asr

@@ -234,11 +234,12 @@ def encoder_output(seed: int, index: int, d_model: int, device="cpu"):
     return grid_values(seed, 1_000_000 + index, (N_AUDIO_CTX, d_model), 221, 7, device)
 
 
-def self_kv_prefix(seed: int, index: int, n_layers: int, n_head: int, length: int,
-                   d_head: int = 64, device="cpu"):
-    """Synthetic pre-filled self-attention cache [L][2][H][length][64], std ~0.7."""
-    return grid_values(seed, 2_000_000 + index, (n_layers, 2, n_head, length, d_head), 155, 7,
-                       device)
+def self_kv_prefix(seed: int, index: int, n_layers: int, n_head: int, d_head: int = 64,
+                   device="cpu"):
+    """Synthetic self-attention cache [L][2][H][448][64], std ~0.7; a sequence
+    with a pre-filled length L uses positions [0, L)."""
+    return grid_values(seed, 2_000_000 + index, (n_layers, 2, n_head, N_TEXT_CTX, d_head), 155,
+                       7, device)
 
 
 # ----------------------------------------------------------------------------
