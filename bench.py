@@ -164,8 +164,8 @@ def main():
     gemm_tflops = g["flops"] / (g["ms"] * 1e-3) / 1e12 if g["ms"] else 0.0
     da = tm["dattn"]
     dattn_gbs = da["bytes"] / (da["ms"] * 1e-3) / 1e9 if da["ms"] else 0.0
-    enc_flops = tm["gemm"]["flops"] + tm["attn"]["flops"]
-    dec_bytes = tm["dgemm"]["bytes"] + tm["dattn"]["bytes"] + tm["vocab"]["bytes"]
+    enc_flops = (tm["gemm"]["flops"] + tm["attn"]["flops"]) / args.steps
+    dec_bytes = (tm["dgemm"]["bytes"] + tm["dattn"]["bytes"] + tm["vocab"]["bytes"]) / args.steps
     kernels = {k: {"ms_per_step": v["ms"] / args.steps, "launches_per_step": v["launches"] / args.steps}
                for k, v in tm.items()}
 

@@ -57,67 +57,95 @@ __device__ __forceinline__ int64_t arow_offset(const AView& a, int r) {
 
 // ---------------------------------------------------------------------------
 // bf16 MFMA GEMM
+//
+// Workgroup tile BM x BN x 64 with WM x WN waves, each wave owning a
+// (BM/WM) x (BN/WN) block of 32x32 MFMA tiles whose fp32 accumulators stay in
+// registers for the whole K loop.  Operand tiles are double-buffered in LDS
+// (rows padded to 72 elements so the 16-byte fragment reads of 32 consecutive
+// rows hit distinct banks); the next K tile is fetched into registers while
+// the current one feeds the MFMAs.
+//
+// Tile order is XCD-aware: the hardware deals workgroups round-robin to the
+// 8 XCDs, so block b runs on XCD b % 8.  Each XCD is given one contiguous
+// range of tiles, walked in groups of GM row tiles (column tile outer, row
+// tile inner) so that the A rows and the W columns a group needs stay in that
+// XCD's L2 while its CUs work through them.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int WM, int WN, int KIND>
+constexpr int kXcd = 8;
+
+__device__ __forceinline__ void tile_of(int bid, int n_tiles, int n_tm, int n_tn, int gm,
+                                        int& tm, int& tn) {
+  const int q = n_tiles / kXcd, r = n_tiles % kXcd;
+  const int xcd = bid % kXcd, local = bid / kXcd;
+  const int t = xcd * q + min(xcd, r) + local;           // contiguous range per XCD
+  const int group = t / (gm * n_tn);
+  const int first_tm = group * gm;
+  const int rows = min(gm, n_tm - first_tm);
+  const int in_group = t - group * gm * n_tn;
+  tm = first_tm + in_group % rows;
+  tn = in_group / rows;
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int KIND>
 __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(AView a, const bf16_t* __restrict__ w,
                                                           int M, int N, int K, Epilogue e,
-                                                          int n_tn) {
+                                                          int n_tm, int n_tn, int gm) {
   constexpr int NT = WM * WN * 64;
-  constexpr int BK = 64;
   constexpr int LD = BK + 8;                       // padded LDS row (elements)
   constexpr int TM = BM / WM, TN = BN / WN;
   constexpr int FM = TM / 32, FN = TN / 32;
-  constexpr int CA = BM * 8 / NT, CB = BN * 8 / NT;
-  static_assert(CA * NT == BM * 8 && CB * NT == BN * 8, "tile/threads");
-  __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * LD];
-  __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BN * LD];
+  constexpr int CPR = BK / 8;                      // 16-byte chunks per tile row
+  constexpr int CA = BM * CPR / NT, CB = BN * CPR / NT;
+  constexpr int RSTEP = NT / CPR;                  // rows covered by one pass of the block
+  static_assert(CA * NT == BM * CPR && CB * NT == BN * CPR, "tile/threads");
+  extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
+  bf16_t* As = smem;                               // [2][BM * LD]
+  bf16_t* Bs = smem + 2 * BM * LD;                 // [2][BN * LD]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave % WM, wn = wave / WM;
-  const int tn = blockIdx.x % n_tn, tm = blockIdx.x / n_tn;
+  int tm, tn;
+  tile_of(blockIdx.x, n_tm * n_tn, n_tm, n_tn, gm, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
 
-  const bf16_t* aptr[CA];
-  bool aok[CA];
-  int arow[CA], akc[CA];
+  // loader geometry: thread t moves 16-byte chunk t % CPR of rows t/CPR + i*RSTEP
+  const int lrow0 = tid / CPR, lkc = (tid % CPR) * 8;
+  const bf16_t* abase = (const bf16_t*)a.ptr;
+  int64_t aoff[CA];
 #pragma unroll
   for (int i = 0; i < CA; ++i) {
-    int c = tid + i * NT;
-    arow[i] = c >> 3;
-    akc[i] = (c & 7) * 8;
-    int r = m0 + arow[i];
-    aok[i] = r < M;
-    aptr[i] = (const bf16_t*)a.ptr + arow_offset(a, aok[i] ? r : 0) + akc[i];
+    int r = min(m0 + lrow0 + i * RSTEP, M - 1);    // rows past M load row M-1, never stored
+    int g = r / a.rows_per_batch;
+    aoff[i] = (int64_t)g * a.batch_stride + (int64_t)(r - g * a.rows_per_batch) * a.lda + lkc;
   }
-  const bf16_t* bptr[CB];
-  bool bok[CB];
-  int brow[CB], bkc[CB];
+  int64_t boff[CB];
 #pragma unroll
-  for (int i = 0; i < CB; ++i) {
-    int c = tid + i * NT;
-    brow[i] = c >> 3;
-    bkc[i] = (c & 7) * 8;
-    int n = n0 + brow[i];
-    bok[i] = n < N;
-    bptr[i] = w + (int64_t)(bok[i] ? n : 0) * K + bkc[i];
-  }
+  for (int i = 0; i < CB; ++i) boff[i] = (int64_t)min(n0 + lrow0 + i * RSTEP, N - 1) * K + lkc;
 
   uint4 ra[CA], rb[CB];
-  const uint4 z = {0u, 0u, 0u, 0u};
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < CA; ++i)
-      ra[i] = (aok[i] && k0 + akc[i] < K) ? *(const uint4*)(aptr[i] + k0) : z;
-#pragma unroll
-    for (int i = 0; i < CB; ++i)
-      rb[i] = (bok[i] && k0 + bkc[i] < K) ? *(const uint4*)(bptr[i] + k0) : z;
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < CA; ++i) *(uint4*)&As[buf][arow[i] * LD + akc[i]] = ra[i];
-#pragma unroll
-    for (int i = 0; i < CB; ++i) *(uint4*)&Bs[buf][brow[i] * LD + bkc[i]] = rb[i];
-  };
+  const int nk = (K + BK - 1) / BK;
+  const bool ktail = (K % BK) != 0;
+
+#define GEMM_GLOAD(k0)                                                              \
+  do {                                                                              \
+    if (!ktail || (k0) + BK <= K) {                                                 \
+      _Pragma("unroll") for (int i = 0; i < CA; ++i) ra[i] = *(const uint4*)(abase + aoff[i] + (k0)); \
+      _Pragma("unroll") for (int i = 0; i < CB; ++i) rb[i] = *(const uint4*)(w + boff[i] + (k0));     \
+    } else {                                                                        \
+      const bool in = (k0) + lkc < K;                                               \
+      _Pragma("unroll") for (int i = 0; i < CA; ++i)                                \
+        ra[i] = in ? *(const uint4*)(abase + aoff[i] + (k0)) : uint4{0u, 0u, 0u, 0u}; \
+      _Pragma("unroll") for (int i = 0; i < CB; ++i)                                \
+        rb[i] = in ? *(const uint4*)(w + boff[i] + (k0)) : uint4{0u, 0u, 0u, 0u};   \
+    }                                                                               \
+  } while (0)
+#define GEMM_SSTORE(buf)                                                            \
+  do {                                                                              \
+    _Pragma("unroll") for (int i = 0; i < CA; ++i)                                  \
+      *(uint4*)&As[(buf) * BM * LD + (lrow0 + i * RSTEP) * LD + lkc] = ra[i];       \
+    _Pragma("unroll") for (int i = 0; i < CB; ++i)                                  \
+      *(uint4*)&Bs[(buf) * BN * LD + (lrow0 + i * RSTEP) * LD + lkc] = rb[i];       \
+  } while (0)
 
   f32x16 acc[FM][FN];
 #pragma unroll
@@ -127,53 +155,92 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(AView a, const bf16_t
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  const int nk = (K + BK - 1) / BK;
-  gload(0);
-  sstore(0);
+  GEMM_GLOAD(0);
+  GEMM_SSTORE(0);
   __syncthreads();
   const int lrow = lane & 31, lk = (lane >> 5) * 8;
+  const int a_frag = (wm * TM + lrow) * LD + lk;
+  const int b_frag = (wn * TN + lrow) * LD + lk;
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
+    if (kt + 1 < nk) GEMM_GLOAD((kt + 1) * BK);
+    const bf16_t* Ac = As + cur * BM * LD + a_frag;
+    const bf16_t* Bc = Bs + cur * BN * LD + b_frag;
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
       bf16x8 af[FM], bfr[FN];
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
-        af[i] = *(const bf16x8*)&As[cur][(wm * TM + i * 32 + lrow) * LD + kk * 16 + lk];
+      for (int i = 0; i < FM; ++i) af[i] = *(const bf16x8*)(Ac + i * 32 * LD + kk * 16);
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
-        bfr[j] = *(const bf16x8*)&Bs[cur][(wn * TN + j * 32 + lrow) * LD + kk * 16 + lk];
+      for (int j = 0; j < FN; ++j) bfr[j] = *(const bf16x8*)(Bc + j * 32 * LD + kk * 16);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) sstore(cur ^ 1);
+    if (kt + 1 < nk) GEMM_SSTORE(cur ^ 1);
     __syncthreads();
   }
+#undef GEMM_GLOAD
+#undef GEMM_SSTORE
 
-  // C layout of a 32x32 block: lane holds column lane%32 and, for register r,
-  // row 8*(r/4) + 4*(lane/32) + r%4.
+  // Epilogue through LDS, one 32x32 block per wave at a time.  In the MFMA
+  // output layout a lane holds column lane%32 and, for register r, row
+  // 8*(r/4) + 4*(lane/32) + r%4; the block is written to LDS in that layout
+  // and read back as two full rows per instruction, so the (possibly heavy)
+  // epilogue math runs in a short rolled loop and every store covers whole
+  // 32-column row segments.
+  float* stage = (float*)smem + wave * (32 * 33);
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < FN; ++j)
+    for (int j = 0; j < FN; ++j) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        int row = m0 + wm * TM + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        int col = n0 + wn * TN + j * 32 + lrow;
-        if (row < M && col < N) epi_apply<KIND, bf16_t>(e, row, col, acc[i][j][r]);
+      for (int r = 0; r < 16; ++r)
+        stage[((r >> 2) * 8 + (lane >> 5) * 4 + (r & 3)) * 33 + lrow] = acc[i][j][r];
+      __syncthreads();
+      const int rbase = m0 + wm * TM + i * 32, cbase = n0 + wn * TN + j * 32;
+#pragma unroll 2
+      for (int t = 0; t < 16; ++t) {
+        const int rr = t * 2 + (lane >> 5);
+        const int row = rbase + rr, col = cbase + lrow;
+        if (row < M && col < N) epi_apply<KIND, bf16_t>(e, row, col, stage[rr * 33 + lrow]);
       }
+      __syncthreads();
+    }
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int KIND>
+static void launch_gemm_cfg(const AView& a, const bf16_t* w, int M, int N, int K,
+                            const Epilogue& e, hipStream_t s, int gm) {
+  constexpr int LD = BK + 8;
+  constexpr size_t lds0 = (size_t)2 * (BM + BN) * LD * sizeof(bf16_t);
+  constexpr size_t lds_epi = (size_t)WM * WN * 32 * 33 * sizeof(float);
+  constexpr size_t lds = lds0 > lds_epi ? lds0 : lds_epi;
+  auto kfn = k_gemm_bf16<BM, BN, BK, WM, WN, KIND>;
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)lds);
+    attr = true;
+  }
+  int n_tm = (M + BM - 1) / BM, n_tn = (N + BN - 1) / BN;
+  kfn<<<n_tm * n_tn, WM * WN * 64, lds, s>>>(a, w, M, N, K, e, n_tm, n_tn, gm);
 }
 
 template <int KIND>
 static void launch_gemm_bf16(const AView& a, const bf16_t* w, int M, int N, int K,
                              const Epilogue& e, hipStream_t s) {
-  constexpr int BM = 128, BN = 128;
-  int n_tm = (M + BM - 1) / BM, n_tn = (N + BN - 1) / BN;
-  k_gemm_bf16<BM, BN, 2, 2, KIND><<<n_tm * n_tn, 256, 0, s>>>(a, w, M, N, K, e, n_tn);
+  // large products: 256x256 tiles (4 waves of 128x128); small ones keep more
+  // workgroups in flight with 128x128 tiles.
+  // large products: 256x128x32 tiles, 8 waves of 64x64; smaller ones keep
+  // more workgroups in flight with 128x128x32 tiles.
+  long tiles = (long)((M + 255) / 256) * ((N + 127) / 128);
+  if (tiles >= 1024)
+    launch_gemm_cfg<256, 128, 32, 4, 2, KIND>(a, w, M, N, K, e, s, 4);
+  else
+    launch_gemm_cfg<128, 128, 32, 2, 2, KIND>(a, w, M, N, K, e, s, 8);
 }
 
 void gemm_bf16(const AView& a, const bf16_t* w, int M, int N, int K, const Epilogue& e,
