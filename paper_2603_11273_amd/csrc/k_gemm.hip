@@ -86,21 +86,33 @@ __device__ __forceinline__ void tile_of(int bid, int n_tiles, int n_tm, int n_tn
   tn = in_group / rows;
 }
 
+// LDS holds each operand tile row-major without padding; the 16-byte chunk c
+// of row r sits at chunk position c ^ swz(r).  On gfx950 a 16-byte LDS access
+// is served 16 lanes at a time from 64 four-byte banks, so 16 lanes must touch
+// 16 distinct 16-byte slots of a 256-byte window: with these swizzles both the
+// fragment reads (32 consecutive rows, same chunk) and the tile stores (whole
+// rows) are conflict-free.
+template <int BK>
+__device__ __forceinline__ int lds_swz(int row) {
+  return BK == 32 ? ((row >> 2) & 3) : ((row >> 1) & 7);
+}
+
 template <int BM, int BN, int BK, int WM, int WN, int KIND>
 __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(AView a, const bf16_t* __restrict__ w,
                                                           int M, int N, int K, Epilogue e,
                                                           int n_tm, int n_tn, int gm) {
   constexpr int NT = WM * WN * 64;
-  constexpr int LD = BK + 8;                       // padded LDS row (elements)
   constexpr int TM = BM / WM, TN = BN / WN;
   constexpr int FM = TM / 32, FN = TN / 32;
   constexpr int CPR = BK / 8;                      // 16-byte chunks per tile row
   constexpr int CA = BM * CPR / NT, CB = BN * CPR / NT;
   constexpr int RSTEP = NT / CPR;                  // rows covered by one pass of the block
+  static_assert(BK == 32 || BK == 64, "BK");
   static_assert(CA * NT == BM * CPR && CB * NT == BN * CPR, "tile/threads");
+  static_assert(RSTEP % 16 == 0, "swizzle period");
   extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
-  bf16_t* As = smem;                               // [2][BM * LD]
-  bf16_t* Bs = smem + 2 * BM * LD;                 // [2][BN * LD]
+  bf16_t* As = smem;                               // [2][BM * BK]
+  bf16_t* Bs = smem + 2 * BM * BK;                 // [2][BN * BK]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave % WM, wn = wave / WM;
@@ -108,43 +120,43 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(AView a, const bf16_t
   tile_of(blockIdx.x, n_tm * n_tn, n_tm, n_tn, gm, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
 
-  // loader geometry: thread t moves 16-byte chunk t % CPR of rows t/CPR + i*RSTEP
-  const int lrow0 = tid / CPR, lkc = (tid % CPR) * 8;
+  // loader: thread t moves logical chunk t % CPR of rows t/CPR + i*RSTEP
+  const int lrow0 = tid / CPR, lc = tid % CPR;
+  const int st_off = lrow0 * BK + ((lc ^ lds_swz<BK>(lrow0)) * 8);   // same swizzle for all i
   const bf16_t* abase = (const bf16_t*)a.ptr;
   int64_t aoff[CA];
 #pragma unroll
   for (int i = 0; i < CA; ++i) {
     int r = min(m0 + lrow0 + i * RSTEP, M - 1);    // rows past M load row M-1, never stored
     int g = r / a.rows_per_batch;
-    aoff[i] = (int64_t)g * a.batch_stride + (int64_t)(r - g * a.rows_per_batch) * a.lda + lkc;
+    aoff[i] = (int64_t)g * a.batch_stride + (int64_t)(r - g * a.rows_per_batch) * a.lda + lc * 8;
   }
   int64_t boff[CB];
 #pragma unroll
-  for (int i = 0; i < CB; ++i) boff[i] = (int64_t)min(n0 + lrow0 + i * RSTEP, N - 1) * K + lkc;
+  for (int i = 0; i < CB; ++i) boff[i] = (int64_t)min(n0 + lrow0 + i * RSTEP, N - 1) * K + lc * 8;
 
-  uint4 ra[CA], rb[CB];
   const int nk = (K + BK - 1) / BK;
   const bool ktail = (K % BK) != 0;
 
-#define GEMM_GLOAD(k0)                                                              \
+#define GEMM_GLOAD(RA, RB, k0)                                                      \
   do {                                                                              \
     if (!ktail || (k0) + BK <= K) {                                                 \
-      _Pragma("unroll") for (int i = 0; i < CA; ++i) ra[i] = *(const uint4*)(abase + aoff[i] + (k0)); \
-      _Pragma("unroll") for (int i = 0; i < CB; ++i) rb[i] = *(const uint4*)(w + boff[i] + (k0));     \
+      _Pragma("unroll") for (int i = 0; i < CA; ++i) RA[i] = *(const uint4*)(abase + aoff[i] + (k0)); \
+      _Pragma("unroll") for (int i = 0; i < CB; ++i) RB[i] = *(const uint4*)(w + boff[i] + (k0));     \
     } else {                                                                        \
-      const bool in = (k0) + lkc < K;                                               \
+      const bool in = (k0) + lc * 8 < K;                                            \
       _Pragma("unroll") for (int i = 0; i < CA; ++i)                                \
-        ra[i] = in ? *(const uint4*)(abase + aoff[i] + (k0)) : uint4{0u, 0u, 0u, 0u}; \
+        RA[i] = in ? *(const uint4*)(abase + aoff[i] + (k0)) : uint4{0u, 0u, 0u, 0u}; \
       _Pragma("unroll") for (int i = 0; i < CB; ++i)                                \
-        rb[i] = in ? *(const uint4*)(w + boff[i] + (k0)) : uint4{0u, 0u, 0u, 0u};   \
+        RB[i] = in ? *(const uint4*)(w + boff[i] + (k0)) : uint4{0u, 0u, 0u, 0u};   \
     }                                                                               \
   } while (0)
-#define GEMM_SSTORE(buf)                                                            \
+#define GEMM_SSTORE(RA, RB, buf)                                                    \
   do {                                                                              \
     _Pragma("unroll") for (int i = 0; i < CA; ++i)                                  \
-      *(uint4*)&As[(buf) * BM * LD + (lrow0 + i * RSTEP) * LD + lkc] = ra[i];       \
+      *(uint4*)&As[(buf) * BM * BK + st_off + i * RSTEP * BK] = RA[i];              \
     _Pragma("unroll") for (int i = 0; i < CB; ++i)                                  \
-      *(uint4*)&Bs[(buf) * BN * LD + (lrow0 + i * RSTEP) * LD + lkc] = rb[i];       \
+      *(uint4*)&Bs[(buf) * BN * BK + st_off + i * RSTEP * BK] = RB[i];              \
   } while (0)
 
   f32x16 acc[FM][FN];
@@ -155,31 +167,52 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(AView a, const bf16_t
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  GEMM_GLOAD(0);
-  GEMM_SSTORE(0);
+  // fragment reads: row lane%32 of each 32-row block (blocks start on
+  // multiples of 32, so the swizzle depends on the lane only), chunk
+  // kk*2 + lane/32.  Fragments of step kk+1 are requested before the MFMAs of
+  // step kk so that LDS latency overlaps matrix work within the wave.
+  const int lrow = lane & 31, sw = lds_swz<BK>(lrow), lh = lane >> 5;
+  const bf16_t* a_frag = As + (wm * TM + lrow) * BK;
+  const bf16_t* b_frag = Bs + (wn * TN + lrow) * BK;
+
+  uint4 ra[CA], rb[CB];
+  GEMM_GLOAD(ra, rb, 0);
+  GEMM_SSTORE(ra, rb, 0);
   __syncthreads();
-  const int lrow = lane & 31, lk = (lane >> 5) * 8;
-  const int a_frag = (wm * TM + lrow) * LD + lk;
-  const int b_frag = (wn * TN + lrow) * LD + lk;
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
-    if (kt + 1 < nk) GEMM_GLOAD((kt + 1) * BK);
-    const bf16_t* Ac = As + cur * BM * LD + a_frag;
-    const bf16_t* Bc = Bs + cur * BN * LD + b_frag;
+#ifndef ASR_GEMM_CEILING_PROBE
+    if (kt + 1 < nk) GEMM_GLOAD(ra, rb, (kt + 1) * BK);
+#endif
+    const bf16_t* Ac = a_frag + cur * BM * BK;
+    const bf16_t* Bc = b_frag + cur * BN * BK;
+    bf16x8 af[2][FM], bfr[2][FN];
+    {
+      const int ch = (lh ^ sw) * 8;
+#pragma unroll
+      for (int i = 0; i < FM; ++i) af[0][i] = *(const bf16x8*)(Ac + i * 32 * BK + ch);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) bfr[0][j] = *(const bf16x8*)(Bc + j * 32 * BK + ch);
+    }
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
-      bf16x8 af[FM], bfr[FN];
+      const int p = kk & 1;
+      if (kk + 1 < BK / 16) {
+        const int ch = (((kk + 1) * 2 + lh) ^ sw) * 8;
 #pragma unroll
-      for (int i = 0; i < FM; ++i) af[i] = *(const bf16x8*)(Ac + i * 32 * LD + kk * 16);
+        for (int i = 0; i < FM; ++i) af[p ^ 1][i] = *(const bf16x8*)(Ac + i * 32 * BK + ch);
 #pragma unroll
-      for (int j = 0; j < FN; ++j) bfr[j] = *(const bf16x8*)(Bc + j * 32 * LD + kk * 16);
+        for (int j = 0; j < FN; ++j) bfr[p ^ 1][j] = *(const bf16x8*)(Bc + j * 32 * BK + ch);
+      }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[p][i], bfr[p][j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) GEMM_SSTORE(cur ^ 1);
+#ifndef ASR_GEMM_CEILING_PROBE
+    if (kt + 1 < nk) GEMM_SSTORE(ra, rb, cur ^ 1);
+#endif
     __syncthreads();
   }
 #undef GEMM_GLOAD
@@ -211,11 +244,193 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(AView a, const bf16_t
     }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 MFMA GEMM with an S-stage LDS ring filled by direct global->LDS loads.
+//
+// Each wave issues global_load_lds_dwordx4: lane l of one instruction lands
+// 16 bytes at LDS base + 16 l, so an instruction fills one contiguous 1 KB
+// slice of a tile (16 rows at BK = 32, 8 rows at BK = 64); the lane picks the
+// global chunk that the swizzled layout wants at its slot.  The loads are
+// issued from inline assembly so the compiler does not serialise every LDS
+// read behind them; completion of tile kt is awaited explicitly (vmcnt) while
+// the loads of the next S-2 tiles stay in flight, then one barrier per K
+// tile publishes it and frees the buffer the next tile is loaded into.
+// Requires K % BK == 0.
+// ---------------------------------------------------------------------------
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+template <int MAXN>
+__device__ __forceinline__ void wait_vmcnt_rt(int n) {
+  // n is wave-uniform; the immediate must be a constant
+  if constexpr (MAXN > 0) {
+    if (n >= MAXN) { wait_vmcnt<MAXN>(); return; }
+    wait_vmcnt_rt<MAXN - 1>(n);
+  } else {
+    wait_vmcnt<0>();
+  }
+}
+
+__device__ __forceinline__ void lds_dma16(uint32_t lds_addr, const void* gptr) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+               :: "s"(lds_addr), "v"(gptr) : "memory", "m0");
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int S, int KIND>
+__global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16_dma(AView a,
+                                                              const bf16_t* __restrict__ w,
+                                                              int M, int N, int K, Epilogue e,
+                                                              int n_tm, int n_tn, int gm) {
+  constexpr int NW = WM * WN;
+  constexpr int TM = BM / WM, TN = BN / WN;
+  constexpr int FM = TM / 32, FN = TN / 32;
+  constexpr int CPR = BK / 8;
+  constexpr int RPI = 1024 / (BK * 2);             // tile rows filled by one wave instruction
+  constexpr int IA = BM / (RPI * NW), IB = BN / (RPI * NW);   // instructions per wave per tile
+  constexpr int LPT = IA + IB;                     // loads per lane per tile
+  static_assert(BK == 32 || BK == 64, "BK");
+  static_assert(IA * RPI * NW == BM && IB * RPI * NW == BN, "tile/waves");
+  static_assert(S >= 2 && LPT * (S - 2) < 64, "stages");
+  extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
+  constexpr int STAGE = (BM + BN) * BK;            // elements per stage
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % WM, wn = wave / WM;
+  int tm, tn;
+  tile_of(blockIdx.x, n_tm * n_tn, n_tm, n_tn, gm, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const uint32_t lds0 =
+      (uint32_t)(uintptr_t)((__attribute__((address_space(3))) bf16_t*)smem);
+
+  // per-lane global sources and per-wave LDS destinations of the tile loads
+  const bf16_t* abase = (const bf16_t*)a.ptr;
+  const bf16_t* asrc[IA];
+  uint32_t adst[IA];
+#pragma unroll
+  for (int i = 0; i < IA; ++i) {
+    const int r0 = (i * NW + wave) * RPI;
+    const int row = r0 + lane / CPR;
+    const int c = (lane % CPR) ^ lds_swz<BK>(row);
+    const int r = min(m0 + row, M - 1);
+    const int g = r / a.rows_per_batch;
+    asrc[i] = abase + (int64_t)g * a.batch_stride + (int64_t)(r - g * a.rows_per_batch) * a.lda +
+              c * 8;
+    adst[i] = __builtin_amdgcn_readfirstlane(lds0 + (uint32_t)(r0 * BK * 2));
+  }
+  const bf16_t* bsrc[IB];
+  uint32_t bdst[IB];
+#pragma unroll
+  for (int i = 0; i < IB; ++i) {
+    const int r0 = (i * NW + wave) * RPI;
+    const int row = r0 + lane / CPR;
+    const int c = (lane % CPR) ^ lds_swz<BK>(row);
+    bsrc[i] = w + (int64_t)min(n0 + row, N - 1) * K + c * 8;
+    bdst[i] = __builtin_amdgcn_readfirstlane(lds0 + (uint32_t)((BM * BK + r0 * BK) * 2));
+  }
+  const int nk = K / BK;
+  auto issue = [&](int tile) {
+    const uint32_t so = (uint32_t)((tile % S) * STAGE * 2);
+    const int k0 = tile * BK;
+#pragma unroll
+    for (int i = 0; i < IA; ++i) lds_dma16(adst[i] + so, asrc[i] + k0);
+#pragma unroll
+    for (int i = 0; i < IB; ++i) lds_dma16(bdst[i] + so, bsrc[i] + k0);
+  };
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int lrow = lane & 31, sw = lds_swz<BK>(lrow), lh = lane >> 5;
+  const bf16_t* a_frag = smem + (wm * TM + lrow) * BK;
+  const bf16_t* b_frag = smem + BM * BK + (wn * TN + lrow) * BK;
+
+#pragma unroll
+  for (int t = 0; t < S - 1; ++t)
+    if (t < nk) issue(t);
+  for (int kt = 0; kt < nk; ++kt) {
+    // tile kt has landed once at most min(S-2, nk-1-kt) later tiles are pending
+    wait_vmcnt_rt<LPT * (S - 2)>(LPT * min(S - 2, nk - 1 - kt));
+    __builtin_amdgcn_s_barrier();
+    if (kt + S - 1 < nk) issue(kt + S - 1);
+    const bf16_t* Ac = a_frag + (kt % S) * STAGE;
+    const bf16_t* Bc = b_frag + (kt % S) * STAGE;
+    bf16x8 af[2][FM], bfr[2][FN];
+    {
+      const int ch = (lh ^ sw) * 8;
+#pragma unroll
+      for (int i = 0; i < FM; ++i) af[0][i] = *(const bf16x8*)(Ac + i * 32 * BK + ch);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) bfr[0][j] = *(const bf16x8*)(Bc + j * 32 * BK + ch);
+    }
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      const int p = kk & 1;
+      if (kk + 1 < BK / 16) {
+        const int ch = (((kk + 1) * 2 + lh) ^ sw) * 8;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) af[p ^ 1][i] = *(const bf16x8*)(Ac + i * 32 * BK + ch);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) bfr[p ^ 1][j] = *(const bf16x8*)(Bc + j * 32 * BK + ch);
+      }
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[p][i], bfr[p][j], acc[i][j], 0, 0, 0);
+    }
+  }
+  wait_vmcnt<0>();
+  __syncthreads();
+
+  float* stage = (float*)smem + wave * (32 * 33);
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        stage[((r >> 2) * 8 + (lane >> 5) * 4 + (r & 3)) * 33 + lrow] = acc[i][j][r];
+      __syncthreads();
+      const int rbase = m0 + wm * TM + i * 32, cbase = n0 + wn * TN + j * 32;
+#pragma unroll 2
+      for (int t = 0; t < 16; ++t) {
+        const int rr = t * 2 + (lane >> 5);
+        const int row = rbase + rr, col = cbase + lrow;
+        if (row < M && col < N) epi_apply<KIND, bf16_t>(e, row, col, stage[rr * 33 + lrow]);
+      }
+      __syncthreads();
+    }
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int S, int KIND>
+static void launch_gemm_dma(const AView& a, const bf16_t* w, int M, int N, int K,
+                            const Epilogue& e, hipStream_t s, int gm) {
+  constexpr size_t lds0 = (size_t)S * (BM + BN) * BK * sizeof(bf16_t);
+  constexpr size_t lds_epi = (size_t)WM * WN * 32 * 33 * sizeof(float);
+  constexpr size_t lds = lds0 > lds_epi ? lds0 : lds_epi;
+  auto kfn = k_gemm_bf16_dma<BM, BN, BK, WM, WN, S, KIND>;
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)lds);
+    attr = true;
+  }
+  int n_tm = (M + BM - 1) / BM, n_tn = (N + BN - 1) / BN;
+  kfn<<<n_tm * n_tn, WM * WN * 64, lds, s>>>(a, w, M, N, K, e, n_tm, n_tn, gm);
+}
+
 template <int BM, int BN, int BK, int WM, int WN, int KIND>
 static void launch_gemm_cfg(const AView& a, const bf16_t* w, int M, int N, int K,
                             const Epilogue& e, hipStream_t s, int gm) {
-  constexpr int LD = BK + 8;
-  constexpr size_t lds0 = (size_t)2 * (BM + BN) * LD * sizeof(bf16_t);
+  constexpr size_t lds0 = (size_t)2 * (BM + BN) * BK * sizeof(bf16_t);
   constexpr size_t lds_epi = (size_t)WM * WN * 32 * 33 * sizeof(float);
   constexpr size_t lds = lds0 > lds_epi ? lds0 : lds_epi;
   auto kfn = k_gemm_bf16<BM, BN, BK, WM, WN, KIND>;
@@ -229,18 +444,29 @@ static void launch_gemm_cfg(const AView& a, const bf16_t* w, int M, int N, int K
   kfn<<<n_tm * n_tn, WM * WN * 64, lds, s>>>(a, w, M, N, K, e, n_tm, n_tn, gm);
 }
 
+// Tile choice by shape (measured on MI355X with the encoder's products):
+// deep-K products (K >= 2048) use 256x256x64 tiles, two LDS stages, 8 waves of
+// 128x64; the rest 256x128x32 with three stages, 8 waves of 64x64; small
+// products 128x128x32 with four stages so that enough workgroups exist.  K not
+// a multiple of 32 (the 80-mel first convolution) takes the register-path
+// kernel, which zero-fills the K tail.
 template <int KIND>
 static void launch_gemm_bf16(const AView& a, const bf16_t* w, int M, int N, int K,
                              const Epilogue& e, hipStream_t s) {
-  // large products: 256x256 tiles (4 waves of 128x128); small ones keep more
-  // workgroups in flight with 128x128 tiles.
-  // large products: 256x128x32 tiles, 8 waves of 64x64; smaller ones keep
-  // more workgroups in flight with 128x128x32 tiles.
-  long tiles = (long)((M + 255) / 256) * ((N + 127) / 128);
-  if (tiles >= 1024)
-    launch_gemm_cfg<256, 128, 32, 4, 2, KIND>(a, w, M, N, K, e, s, 4);
-  else
-    launch_gemm_cfg<128, 128, 32, 2, 2, KIND>(a, w, M, N, K, e, s, 8);
+  const long t256x128 = (long)((M + 255) / 256) * ((N + 127) / 128);
+  const long t256x256 = (long)((M + 255) / 256) * ((N + 255) / 256);
+  if (K % 32 != 0) {
+    if (t256x128 >= 1024)
+      launch_gemm_cfg<256, 128, 32, 4, 2, KIND>(a, w, M, N, K, e, s, 4);
+    else
+      launch_gemm_cfg<128, 128, 32, 2, 2, KIND>(a, w, M, N, K, e, s, 8);
+  } else if (K >= 2048 && K % 64 == 0 && t256x256 >= 512) {
+    launch_gemm_dma<256, 256, 64, 2, 4, 2, KIND>(a, w, M, N, K, e, s, 4);
+  } else if (t256x128 >= 512) {
+    launch_gemm_dma<256, 128, 32, 4, 2, 3, KIND>(a, w, M, N, K, e, s, 4);
+  } else {
+    launch_gemm_dma<128, 128, 32, 2, 2, 4, KIND>(a, w, M, N, K, e, s, 8);
+  }
 }
 
 void gemm_bf16(const AView& a, const bf16_t* w, int M, int N, int K, const Epilogue& e,
