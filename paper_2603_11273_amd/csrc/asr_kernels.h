@@ -42,7 +42,12 @@ enum EpiKind : int32_t {
   EPI_CONV1 = 3,      // h1[g][t+1][n] = gelu(acc + bias[n]); h1[g][0][n] = 0 (storage)
   EPI_CONV2 = 4,      // x[r][n] = gelu(acc + bias[n]) + pos[r % 1500][n]   (float32)
   EPI_XKV = 5,        // cross cache of slot[g], all decoder layers        (storage)
+  EPI_QKV = 6,        // q, k -> out[r][n] (n < 2d); v -> out2 = V^T per head (storage)
 };
+
+// Row stride (positions) of the per-head transposed V written by EPI_QKV:
+// V^T[b][h][dim][kVtLd], positions 1500..1535 stay zero.
+constexpr int kVtLd = 1536;
 
 struct Epilogue {
   int32_t kind;
@@ -52,8 +57,9 @@ struct Epilogue {
   const float* pos;     // CONV2: sinusoid table [1500][N]
   const int32_t* slots; // XKV: slot of each clip
   int64_t slot_stride;  // XKV: elements per slot's cross cache
-  int32_t d_model;      // XKV / CONV1
-  int32_t n_head;       // XKV
+  int32_t d_model;      // XKV / CONV1 / QKV
+  int32_t n_head;       // XKV / QKV
+  void* out2;           // QKV: transposed V [B][H][64][kVtLd]
 };
 
 // Dense GEMM C[M][N] = A[M][K] . W[N][K]^T with a fused epilogue.
@@ -90,7 +96,8 @@ void layer_norm(const float* x, int rows, int d, const float* g, const float* b,
                 hipStream_t s);
 
 // Encoder self-attention over 1500 positions, qkv [B*1500][3d], out [B*1500][d].
-void flash_attn_bf16(const bf16_t* qkv, bf16_t* out, int B, int n_head, hipStream_t s);
+void flash_attn_bf16(const bf16_t* qkv, const bf16_t* vt, bf16_t* out, int B, int n_head,
+                     hipStream_t s);
 void flash_attn_f32(const float* qkv, float* out, int B, int n_head, hipStream_t s);
 
 // Decode attention.  Self: writes k, v of each row at its slot position, then

@@ -28,52 +28,96 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
 
 // ---------------------------------------------------------------------------
 // Encoder flash attention (bf16)
+//
+// Block = 4 waves x 64 queries of one (clip, head); tiles of 64 keys.  K
+// comes from the fused QKV buffer, V from the per-head transposed copy the
+// QKV GEMM writes (V^T[dim][position], zero past 1500), so both tiles are
+// plain 16-byte row copies into LDS (XOR-swizzled rows, conflict-free).
+// S^T = K Q^T is computed per 32-key x 32-query block: in the MFMA output
+// layout a lane owns one query and 16 keys, so the row max needs one
+// cross-lane exchange (lane ^ 32), the probabilities (bf16) are directly the
+// B operand of O^T += V^T P^T, and the online-softmax rescale is per lane.
+// The K and V^T fragments read from LDS serve both 32-query groups of a
+// wave.  The 1/sqrt(64) scale and log2(e) fold into one FMA before exp2;
+// only the last key tile needs the position mask.
 // ---------------------------------------------------------------------------
 constexpr int FA_KT = 64;          // keys per tile
-constexpr int FA_LD = 64 + 8;      // padded LDS row
 
-__global__ __launch_bounds__(256) void k_flash_bf16(const bf16_t* __restrict__ qkv,
-                                                    bf16_t* __restrict__ out, int n_head) {
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[FA_KT * FA_LD];   // [key][dim]
-  __shared__ __attribute__((aligned(16))) bf16_t Vt[64 * FA_LD];      // [dim][key]
+__device__ __forceinline__ int fa_swz(int row) { return (row >> 1) & 7; }
+
+template <int NW>
+__global__ __launch_bounds__(NW * 64) void k_flash_bf16(const bf16_t* __restrict__ qkv,
+                                                       const bf16_t* __restrict__ vt,
+                                                       bf16_t* __restrict__ out, int n_head) {
+  constexpr int NTH = NW * 64;
+  constexpr int CPT = 512 / NTH;                   // 16-byte chunks per thread per operand tile
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][FA_KT * 64];   // [key][dim]
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[2][64 * FA_KT];   // [dim][key]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = blockIdx.y, b = blockIdx.z;
   const int d = n_head * 64, ld3 = 3 * d;
   const bf16_t* base = qkv + (int64_t)b * kCtx * ld3;
-  const int qrow = blockIdx.x * 128 + wave * 32 + (lane & 31);
-  const bool qvalid = qrow < kCtx;
-  const int half = lane >> 5;
+  const bf16_t* vbase = vt + ((int64_t)b * n_head + h) * 64 * kVtLd;
+  const int half = lane >> 5, l32 = lane & 31;
+  const int q = blockIdx.x * (NW * 32) + wave * 32 + l32;   // this lane's query
   const uint4 z = {0u, 0u, 0u, 0u};
 
+  // Q fragments (B operand of S^T): dims kk*16 + half*8 .. +8 of query q
   bf16x8 qf[4];
   {
-    const bf16_t* qp = base + (int64_t)(qvalid ? qrow : 0) * ld3 + h * 64 + half * 8;
+    const bf16_t* qp = base + (int64_t)(q < kCtx ? q : 0) * ld3 + h * 64 + half * 8;
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
-      qf[kk] = as_bf16x8(qvalid ? *(const uint4*)(qp + kk * 16) : z);
+    for (int kk = 0; kk < 4; ++kk) {
+      uint4 v = z;
+      if (q < kCtx) v = *(const uint4*)(qp + kk * 16);
+      qf[kk] = as_bf16x8(v);
+    }
   }
-  f32x16 o0, o1;
+
+  // tile loader: chunk c of K (rows = keys) and of V^T (rows = dims); a chunk
+  // is 8 consecutive elements of one 64-element row
+  uint4 rk[CPT], rv[CPT];
+#define FA_GLOAD(k0)                                                                \
+  do {                                                                              \
+    _Pragma("unroll") for (int u = 0; u < CPT; ++u) {                               \
+      const int c = tid + u * NTH, row = c >> 3, ch = c & 7;                        \
+      const int key = (k0) + row;                                                   \
+      rk[u] = z;                                                                    \
+      if (key < kCtx) rk[u] = *(const uint4*)(base + (int64_t)key * ld3 + d + h * 64 + ch * 8); \
+      rv[u] = *(const uint4*)(vbase + (int64_t)row * kVtLd + (k0) + ch * 8);        \
+    }                                                                               \
+  } while (0)
+  // V^T rows 16..31 (mod 32) keep their two 8-byte halves swapped, so the
+  // 8-byte fragment reads of 32 consecutive rows hit distinct banks
+#define FA_SSTORE(buf)                                                              \
+  do {                                                                              \
+    _Pragma("unroll") for (int u = 0; u < CPT; ++u) {                               \
+      const int c = tid + u * NTH, row = c >> 3, ch = c & 7;                        \
+      const int pos = row * 64 + ((ch ^ fa_swz(row)) * 8);                          \
+      *(uint4*)&Ks[buf][pos] = rk[u];                                               \
+      const uint4 v = rv[u];                                                        \
+      *(uint4*)&Vs[buf][pos] = (row & 16) ? uint4{v.z, v.w, v.x, v.y} : v;          \
+    }                                                                               \
+  } while (0)
+
+  f32x16 o0, o1;                                   // O^T dims 0..31, 32..63
 #pragma unroll
   for (int r = 0; r < 16; ++r) o0[r] = o1[r] = 0.f;
   float m = -INFINITY, l = 0.f;
-  const float sc = 0.125f * 1.4426950408889634f;     // 1/sqrt(64) * log2(e)
+  const float sc = 0.125f * 1.4426950408889634f;  // 1/sqrt(64) * log2(e)
+  const int sw = fa_swz(l32);
+  const int vhalf = (half ^ ((l32 >> 4) & 1)) * 4;
 
-  for (int k0 = 0; k0 < kCtx; k0 += FA_KT) {
-    for (int c = tid; c < FA_KT * 8; c += 256) {
-      int key = c >> 3, dc = (c & 7) * 8;
-      int gk = k0 + key;
-      uint4 kv = z, vv = z;
-      if (gk < kCtx) {
-        const bf16_t* rp = base + (int64_t)gk * ld3 + h * 64 + dc;
-        kv = *(const uint4*)(rp + d);
-        vv = *(const uint4*)(rp + 2 * d);
-      }
-      *(uint4*)&Ks[key * FA_LD + dc] = kv;
-      const bf16_t* ve = (const bf16_t*)&vv;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) Vt[(dc + i) * FA_LD + key] = ve[i];
-    }
-    __syncthreads();
+  constexpr int NT = (kCtx + FA_KT - 1) / FA_KT;
+  FA_GLOAD(0);
+  FA_SSTORE(0);
+  __syncthreads();
+  for (int kt = 0; kt < NT; ++kt) {
+    const int cur = kt & 1;
+    const int k0 = kt * FA_KT;
+    if (kt + 1 < NT) FA_GLOAD(k0 + FA_KT);
+    const bf16_t* Kc = Ks[cur];
+    const bf16_t* Vc = Vs[cur];
 
     f32x16 s[2];
 #pragma unroll
@@ -82,27 +126,32 @@ __global__ __launch_bounds__(256) void k_flash_bf16(const bf16_t* __restrict__ q
       for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
-        bf16x8 kf = *(const bf16x8*)&Ks[(kb * 32 + (lane & 31)) * FA_LD + kk * 16 + half * 8];
+        const bf16x8 kf =
+            *(const bf16x8*)(Kc + (kb * 32 + l32) * 64 + (((kk * 2 + half) ^ sw) * 8));
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[kb], 0, 0, 0);
       }
     }
-    // s[kb][r]: key k0 + 32 kb + 8 (r/4) + 4 half + r%4, query qrow
+    if (k0 + FA_KT > kCtx) {                       // last tile: keys past 1500 do not exist
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = k0 + kb * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
+          if (key >= kCtx) s[kb][r] = -INFINITY;
+        }
+    }
     float tmax = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        int key = k0 + kb * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
-        float v = key < kCtx ? s[kb][r] * sc : -INFINITY;
-        s[kb][r] = v;
-        tmax = fmaxf(tmax, v);
-      }
+      for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, s[kb][r]);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
     const float mnew = fmaxf(m, tmax);
-    const float alpha = exp2f(m - mnew);
+    const float alpha = exp2f((m - mnew) * sc);
+    const float nb = -mnew * sc;
     m = mnew;
     float psum = 0.f;
-    bf16x8 pb[2][2];
+    bf16x8 pb[2][2];                               // [kb][hf]
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -110,7 +159,7 @@ __global__ __launch_bounds__(256) void k_flash_bf16(const bf16_t* __restrict__ q
         float p[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          p[i] = exp2f(s[kb][hf * 8 + i] - mnew);
+          p[i] = exp2f(fmaf(s[kb][hf * 8 + i], sc, nb));
           psum += p[i];
         }
         uint4 u = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
@@ -127,25 +176,31 @@ __global__ __launch_bounds__(256) void k_flash_bf16(const bf16_t* __restrict__ q
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
-        const int kbase = kb * 32 + hf * 16 + half * 4;
-        const bf16_t* v0 = &Vt[(lane & 31) * FA_LD + kbase];
-        const bf16_t* v1 = &Vt[(32 + (lane & 31)) * FA_LD + kbase];
-        uint2 a0 = *(const uint2*)v0, a1 = *(const uint2*)(v0 + 8);
-        uint2 c0 = *(const uint2*)v1, c1 = *(const uint2*)(v1 + 8);
-        bf16x8 vf0 = as_bf16x8(uint4{a0.x, a0.y, a1.x, a1.y});
-        bf16x8 vf1 = as_bf16x8(uint4{c0.x, c0.y, c1.x, c1.y});
-        o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf0, pb[kb][hf], o0, 0, 0, 0);
-        o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf1, pb[kb][hf], o1, 0, 0, 0);
+        // keys kb*32 + hf*16 + half*4 + {0..3} and + 8: chunks c, c+1 of the V^T row
+        const int c = kb * 4 + hf * 2;
+        const bf16_t* v0 = Vc + l32 * 64;
+        const bf16_t* v1 = Vc + (32 + l32) * 64;
+        const uint2 a0 = *(const uint2*)(v0 + ((c ^ sw) * 8) + vhalf);
+        const uint2 a1 = *(const uint2*)(v0 + (((c + 1) ^ sw) * 8) + vhalf);
+        const uint2 c0 = *(const uint2*)(v1 + ((c ^ sw) * 8) + vhalf);
+        const uint2 c1 = *(const uint2*)(v1 + (((c + 1) ^ sw) * 8) + vhalf);
+        o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(uint4{a0.x, a0.y, a1.x, a1.y}),
+                                                     pb[kb][hf], o0, 0, 0, 0);
+        o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(uint4{c0.x, c0.y, c1.x, c1.y}),
+                                                     pb[kb][hf], o1, 0, 0, 0);
       }
+    if (kt + 1 < NT) FA_SSTORE(cur ^ 1);
     __syncthreads();
   }
+#undef FA_GLOAD
+#undef FA_SSTORE
   l += __shfl_xor(l, 32, 64);
-  if (!qvalid) return;
+  if (q >= kCtx) return;
   const float inv = 1.0f / l;
-  bf16_t* op = out + ((int64_t)b * kCtx + qrow) * d + h * 64;
+  bf16_t* op = out + ((int64_t)b * kCtx + q) * d + h * 64;
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
-    int d0 = g * 8 + half * 4;
+    const int d0 = g * 8 + half * 4;
     uint2 w0 = {pack_bf16x2(o0[g * 4 + 0] * inv, o0[g * 4 + 1] * inv),
                 pack_bf16x2(o0[g * 4 + 2] * inv, o0[g * 4 + 3] * inv)};
     uint2 w1 = {pack_bf16x2(o1[g * 4 + 0] * inv, o1[g * 4 + 1] * inv),
@@ -155,10 +210,12 @@ __global__ __launch_bounds__(256) void k_flash_bf16(const bf16_t* __restrict__ q
   }
 }
 
-void flash_attn_bf16(const bf16_t* qkv, bf16_t* out, int B, int n_head, hipStream_t s) {
+void flash_attn_bf16(const bf16_t* qkv, const bf16_t* vt, bf16_t* out, int B, int n_head,
+                     hipStream_t s) {
   if (B <= 0) return;
-  dim3 grid((kCtx + 127) / 128, n_head, B);
-  k_flash_bf16<<<grid, 256, 0, s>>>(qkv, out, n_head);
+  constexpr int NW = 8;
+  dim3 grid((kCtx + NW * 32 - 1) / (NW * 32), n_head, B);
+  k_flash_bf16<NW><<<grid, NW * 64, 0, s>>>(qkv, vt, out, n_head);
 }
 
 // ---------------------------------------------------------------------------

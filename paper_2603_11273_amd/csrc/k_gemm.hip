@@ -47,6 +47,40 @@ __device__ __forceinline__ void epi_apply(const Epilogue& e, int r, int n, float
     int64_t addr = (int64_t)e.slots[g] * e.slot_stride +
                    ((((int64_t)l * 2 + kv) * e.n_head + h) * kCtx + t) * kHeadDim + c;
     St<T>::st((T*)e.out, addr, v);
+  } else if constexpr (KIND == EPI_QKV) {
+    const int two_d = 2 * e.d_model;
+    if (n < two_d) {
+      St<T>::st((T*)e.out, (int64_t)r * e.ldc + n, v);
+    } else {
+      int g = r / kCtx, t = r - g * kCtx;
+      int hd = n - two_d;
+      int64_t addr = (((int64_t)g * e.n_head + (hd >> 6)) * kHeadDim + (hd & 63)) * kVtLd + t;
+      St<T>::st((T*)e.out2, addr, v);
+    }
+  }
+}
+
+// Epilogue of one 32x32 accumulator block staged in LDS (row stride 33).  V
+// blocks of the fused QKV product are walked column-major so that lanes run
+// along positions, the contiguous direction of the transposed V.
+template <int KIND>
+__device__ __forceinline__ void epi_block(const Epilogue& e, const float* stage, int rbase,
+                                          int cbase, int M, int N, int lane) {
+  const int l32 = lane & 31, lh = lane >> 5;
+  if (KIND == EPI_QKV && cbase >= 2 * e.d_model) {
+#pragma unroll 2
+    for (int t = 0; t < 16; ++t) {
+      const int cc = t * 2 + lh;
+      const int row = rbase + l32, col = cbase + cc;
+      if (row < M && col < N) epi_apply<KIND, bf16_t>(e, row, col, stage[l32 * 33 + cc]);
+    }
+  } else {
+#pragma unroll 2
+    for (int t = 0; t < 16; ++t) {
+      const int rr = t * 2 + lh;
+      const int row = rbase + rr, col = cbase + l32;
+      if (row < M && col < N) epi_apply<KIND, bf16_t>(e, row, col, stage[rr * 33 + l32]);
+    }
   }
 }
 
@@ -233,13 +267,7 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(AView a, const bf16_t
       for (int r = 0; r < 16; ++r)
         stage[((r >> 2) * 8 + (lane >> 5) * 4 + (r & 3)) * 33 + lrow] = acc[i][j][r];
       __syncthreads();
-      const int rbase = m0 + wm * TM + i * 32, cbase = n0 + wn * TN + j * 32;
-#pragma unroll 2
-      for (int t = 0; t < 16; ++t) {
-        const int rr = t * 2 + (lane >> 5);
-        const int row = rbase + rr, col = cbase + lrow;
-        if (row < M && col < N) epi_apply<KIND, bf16_t>(e, row, col, stage[rr * 33 + lrow]);
-      }
+      epi_block<KIND>(e, stage, m0 + wm * TM + i * 32, n0 + wn * TN + j * 32, M, N, lane);
       __syncthreads();
     }
 }
@@ -399,13 +427,7 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16_dma(AView a,
       for (int r = 0; r < 16; ++r)
         stage[((r >> 2) * 8 + (lane >> 5) * 4 + (r & 3)) * 33 + lrow] = acc[i][j][r];
       __syncthreads();
-      const int rbase = m0 + wm * TM + i * 32, cbase = n0 + wn * TN + j * 32;
-#pragma unroll 2
-      for (int t = 0; t < 16; ++t) {
-        const int rr = t * 2 + (lane >> 5);
-        const int row = rbase + rr, col = cbase + lrow;
-        if (row < M && col < N) epi_apply<KIND, bf16_t>(e, row, col, stage[rr * 33 + lrow]);
-      }
+      epi_block<KIND>(e, stage, m0 + wm * TM + i * 32, n0 + wn * TN + j * 32, M, N, lane);
       __syncthreads();
     }
 }
@@ -479,6 +501,7 @@ void gemm_bf16(const AView& a, const bf16_t* w, int M, int N, int K, const Epilo
     case EPI_CONV1: launch_gemm_bf16<EPI_CONV1>(a, w, M, N, K, e, s); break;
     case EPI_CONV2: launch_gemm_bf16<EPI_CONV2>(a, w, M, N, K, e, s); break;
     case EPI_XKV: launch_gemm_bf16<EPI_XKV>(a, w, M, N, K, e, s); break;
+    case EPI_QKV: launch_gemm_bf16<EPI_QKV>(a, w, M, N, K, e, s); break;
   }
 }
 

@@ -81,7 +81,8 @@ struct Layout {
   size_t self_kv = 0, cross_kv = 0;
   int64_t self_stride = 0, cross_stride = 0;   // elements per slot
   size_t pcm_stage = 0, pcm_ptrs = 0, pcm_n = 0, mel_raw = 0, clip_max = 0, mel_norm = 0,
-         h1 = 0, x = 0, xn = 0, qkv = 0, att = 0, hid = 0, p_slots = 0;
+         h1 = 0, x = 0, xn = 0, qkv = 0, vt = 0, att = 0, hid = 0, p_slots = 0;
+  size_t vt_bytes = 0;
   size_t d_slots = 0, d_tokens = 0, d_pos = 0, d_h = 0, d_xn = 0, d_qkv = 0, d_q = 0, d_att = 0,
          d_hid = 0, d_partial = 0, d_logits = 0, d_keys = 0, d_argmax = 0, d_flag = 0;
   size_t wstage = 0;
@@ -272,6 +273,10 @@ void plan(asr_ctx* c) {
   L.x = b.take(R * d * f4);
   L.xn = b.take(R * d * es);
   L.qkv = b.take(R * 3 * d * es);
+  // per-head transposed V of the bf16 encoder attention, positions padded to
+  // kVtLd with zeros (written once at bind, never touched by the kernels)
+  L.vt_bytes = c->cfg.dtype == ASR_BF16 ? (size_t)P * H * kHeadDim * kVtLd * es : 0;
+  L.vt = b.take(L.vt_bytes);
   L.att = b.take(R * d * es);
   L.hid = b.take(R * F * es);
   L.p_slots = b.take(P * 4);
@@ -364,6 +369,7 @@ asr_status upload_tables(asr_ctx* c) {
   HIPCHK(hipMemcpyAsync(c->at(c->L.fb_range), rng.data(), rng.size() * 4, hipMemcpyHostToDevice, s));
   HIPCHK(hipMemcpyAsync(c->at(c->L.sinus), sin_tab.data(), sin_tab.size() * 4,
                         hipMemcpyHostToDevice, s));
+  if (c->L.vt_bytes) fill_u32(c->at<uint32_t>(c->L.vt), 0u, (int64_t)(c->L.vt_bytes / 4), s);
   HIPCHK(hipStreamSynchronize(s));
   return ASR_OK;
 }
@@ -539,18 +545,24 @@ asr_status encode_clips(asr_ctx* c, int n) {
     const EncLayer& w = L.enc[l];
     ln_any<T>(c, x, R, w.ln1_g, w.ln1_b, xn);
     {
+      // bf16: q, k into the fused buffer and v transposed per head for the
+      // flash-attention kernel; fp32: plain [R][3d]
       AView a{xn, d, 0, R};
       Epilogue e{};
-      e.kind = EPI_STORE;
+      e.kind = c->bf16() ? EPI_QKV : EPI_STORE;
       e.out = qkv;
       e.ldc = 3 * d;
       e.bias = c->at<float>(w.qkv_b);
+      e.d_model = d;
+      e.n_head = H;
+      e.out2 = c->at(L.vt);
       gemm_any<T>(c, a, w.qkv_w, R, 3 * d, d, e);
     }
     timed(c, ASR_K_ATTN, 4.0 * n * H * (double)kCtx * kCtx * 64,
           (double)R * 4 * d * c->es, [&] {
             if (c->bf16())
-              flash_attn_bf16((const bf16_t*)qkv, (bf16_t*)att, n, H, c->stream);
+              flash_attn_bf16((const bf16_t*)qkv, c->at<bf16_t>(L.vt), (bf16_t*)att, n, H,
+                              c->stream);
             else
               flash_attn_f32((const float*)qkv, (float*)att, n, H, c->stream);
           });
