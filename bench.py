@@ -34,6 +34,22 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "gemm_bf16_large-v3_step_traffic.md")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2603_11273_amd", "csrc", "k_gemm.hip")
+
+
+def gemm_traffic_per_launch():
+    """Counter-measured bytes per GEMM launch, or None once the kernel source
+    differs from the one the counters were taken on."""
+    import hashlib
+    import re
+    try:
+        text = open(TRAFFIC_SUMMARY).read()
+        rec = json.loads(re.search(r"```json\n(.*?)\n```", text, re.S).group(1))
+        sha = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()[:16]
+    except Exception:
+        return None
+    return rec["gemm_bytes_per_launch"] if rec.get("kernel_source_sha256_16") == sha else None
 
 
 def log(msg):
@@ -49,6 +65,13 @@ def parse():
     ap.add_argument("--decode", type=int, default=128)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=25.0)
+    ap.add_argument("--zero-inputs", action="store_true",
+                    help="zero-filled weights, caches and audio instead of the seeded "
+                         "generator: same launches and memory traffic, for hardware-counter "
+                         "runs only (values are meaningless)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy (3 times): the reference "
+                         "reading for the FETCH_SIZE / WRITE_SIZE counters")
     return ap.parse_args()
 
 
@@ -64,6 +87,15 @@ def main():
     import torch
     from paper_2603_11273_amd import asr, synth
 
+    if args.copy_calibration:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")      # 1 GiB
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": src.numel() * 4, "copies": 3}))
+        return
+
     if args.warmup + args.steps > 45:
         raise SystemExit("warmup + steps must stay <= 45 (decode positions stay below 448)")
     P, D = args.prefill, args.decode
@@ -78,7 +110,11 @@ def main():
     log(f"workspace {ctx.workspace_size() / 2**30:.1f} GiB")
     ctx.bind()
     t0 = time.time()
-    params = synth.model_params(shape, enc_wl.seed, device=dev)
+    if args.zero_inputs:
+        params = {n: torch.zeros(shp, dtype=torch.float32, device=dev)
+                  for n, shp, _ in synth.param_specs(shape)}
+    else:
+        params = synth.model_params(shape, enc_wl.seed, device=dev)
     ctx.load_weights(list(params.values()), on_device=True)
     torch.cuda.synchronize()
     log(f"weights generated + loaded in {time.time() - t0:.1f} s")
@@ -103,20 +139,30 @@ def main():
     t0 = time.time()
     for s0 in range(0, D, P):
         idx = list(range(s0, min(D, s0 + P)))
-        E = torch.stack([synth.encoder_output(dec_wl.seed, b, shape.d_model, device=dev)
-                         for b in idx])
+        if args.zero_inputs:
+            E = torch.zeros((len(idx), synth.N_AUDIO_CTX, shape.d_model), device=dev)
+        else:
+            E = torch.stack([synth.encoder_output(dec_wl.seed, b, shape.d_model, device=dev)
+                             for b in idx])
         ctx.debug_set_encoder_out(idx, [-1] * len(idx), [steps_left[b] for b in idx], E,
                                   on_device=True)
         del E
     for b in range(D):
-        kv = synth.self_kv_prefix(dec_wl.seed, b, shape.n_dec, shape.n_head, device=dev)
+        if args.zero_inputs:
+            kv = torch.zeros((shape.n_dec, 2, shape.n_head, synth.N_TEXT_CTX, 64), device=dev)
+        else:
+            kv = synth.self_kv_prefix(dec_wl.seed, b, shape.n_dec, shape.n_head, device=dev)
         ctx.debug_set_self_kv(b, kv, int(kv_len[b]), on_device=True)
         del kv
     torch.cuda.synchronize()
     log(f"{D} decode slots filled in {time.time() - t0:.1f} s")
 
     # -------------------------------------------------- prefill audio in HBM
-    pcm_host = np.stack([synth.pcm_clip(enc_wl.seed, i, synth.N_SAMPLES_30S) for i in range(P)])
+    if args.zero_inputs:
+        pcm_host = np.zeros((P, synth.N_SAMPLES_30S), np.float32)
+    else:
+        pcm_host = np.stack([synth.pcm_clip(enc_wl.seed, i, synth.N_SAMPLES_30S)
+                             for i in range(P)])
     pcm = torch.from_numpy(pcm_host).to(dev)
     toks = synth.token_ids(dec_wl.seed, (args.warmup + args.steps, D), shape.vocab)
     del params
@@ -199,12 +245,16 @@ def main():
         "roofline": {"bound": "mfma", "kernel": "gemm_bf16 (encoder, stem, cross K/V)",
                      "achieved": round(gemm_tflops, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None},
+                     "traffic": gemm_traffic_per_launch(),
+                     "flops_per_launch": round(g["flops"] / max(1, g["launches"])),
+                     "avg_launch_us": round(g["ms"] * 1e3 / max(1, g["launches"]), 1)},
         "roofline_decode": {"bound": "hbm", "kernel": "decode attention (self + cross)",
                             "achieved": round(dattn_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                             "frac": round(dattn_gbs / PEAK_HBM_GBS, 4), "traffic": None},
     }
-    if not args.no_cpu_baseline:
+    if args.zero_inputs:
+        result["data"] = "zero-filled (hardware-counter run; values meaningless)"
+    if not args.no_cpu_baseline and not args.zero_inputs:
         result["cpu_baseline"] = cpu_baseline(shape, enc_wl, dec_wl, pcm_host[0], P, D,
                                               ms_step, args.cpu_budget_s)
     print(json.dumps(result), flush=True)

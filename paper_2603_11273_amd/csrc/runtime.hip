@@ -485,7 +485,12 @@ asr_status run_mel(asr_ctx* c, int n) {
 template <typename T>
 void gemm_any(asr_ctx* c, const AView& a, size_t w_off, int M, int N, int K, const Epilogue& e) {
   double flops = 2.0 * M * N * K;
-  double bytes = (double)M * K * c->es + (double)N * K * c->es + (double)M * N * c->es;
+  // operands read once, result written once; the fp32 residual epilogue also
+  // reads the residual, the second convolution writes fp32
+  double out_bytes = (double)M * N * c->es;
+  if (e.kind == EPI_RESID) out_bytes = 2.0 * M * N * 4;
+  if (e.kind == EPI_CONV2) out_bytes = (double)M * N * 4;
+  double bytes = (double)M * K * c->es + (double)N * K * c->es + out_bytes;
   timed(c, ASR_K_GEMM, flops, bytes, [&] {
     if (c->bf16())
       gemm_bf16(a, c->at<bf16_t>(w_off), M, N, K, e, c->stream);
