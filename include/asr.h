@@ -67,7 +67,7 @@ typedef enum { ASR_F32 = 0, ASR_BF16 = 1 } asr_dtype;
  * residual stream, LayerNorm and softmax; ASR_F32 keeps everything float32. */
 typedef struct {
   int32_t n_mels;      /* 80 or 128 */
-  int32_t d_model;     /* multiple of 64 */
+  int32_t d_model;     /* multiple of 64 (of 128 for bf16), at most 2048 */
   int32_t n_enc;       /* encoder layers (>= 0) */
   int32_t n_dec;       /* decoder layers (>= 0) */
   int32_t n_head;      /* d_model / 64 */
@@ -199,8 +199,14 @@ typedef enum {
   ASR_K_COUNT = 10
 } asr_kernel_class;
 
-/* enable != 0 records an event pair around every launch until disabled. */
-asr_status asr_set_timing(asr_ctx* ctx, int32_t enable);
+/* classes is a bit mask over the asr_kernel_class values: bit k selects class
+ * k, 0 turns timing off, ASR_TIME_ALL times every class.  An event pair is
+ * recorded on the context's stream around every launch (and phase) of a
+ * selected class.  Each pair costs a little queue time, so a step timed with
+ * a mask that selects the many short decode launches runs somewhat slower
+ * than an untimed one. */
+#define ASR_TIME_ALL ((1 << ASR_K_COUNT) - 1)
+asr_status asr_set_timing(asr_ctx* ctx, int32_t classes);
 /* Synchronises, then reports for one class since the last reset: summed
  * kernel milliseconds, launches, algorithmic flops and algorithmic HBM bytes
  * (the minimum traffic the launches need: operands read once, results

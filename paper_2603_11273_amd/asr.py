@@ -21,6 +21,7 @@ F32, BF16 = 0, 1
 K_MEL, K_GEMM, K_ATTN, K_LN, K_DGEMM, K_DATTN, K_VOCAB, K_OTHER, K_PREFILL, K_DECODE = range(10)
 KERNEL_CLASSES = ["mel", "gemm", "attn", "ln", "dgemm", "dattn", "vocab", "other", "prefill",
                   "decode"]
+TIME_ALL = (1 << len(KERNEL_CLASSES)) - 1
 
 EXPORTED = [
     "asr_create", "asr_destroy", "asr_last_error", "asr_workspace_size", "asr_bind",
@@ -258,8 +259,14 @@ class Context:
                 "steps_left": left.value}
 
     # -- timing ---------------------------------------------------------------
-    def set_timing(self, enable: bool):
-        _check(lib.asr_set_timing(self.h, int(enable)))
+    def set_timing(self, classes=True):
+        """True times every kernel class, False none; an int is a bit mask
+        over the class numbers (K_MEL .. K_DECODE)."""
+        if classes is True:
+            classes = TIME_ALL
+        elif classes is False:
+            classes = 0
+        _check(lib.asr_set_timing(self.h, int(classes)))
 
     def reset_timing(self):
         _check(lib.asr_reset_timing(self.h))

@@ -72,12 +72,18 @@ void gemm_f32(const AView& a, const float* w, int M, int N, int K, const Epilogu
 // Returns the number of K-splits used (the partial buffer holds splits*D*N floats).
 int dgemm_bf16(const bf16_t* x, const bf16_t* w, int D, int N, int K, float* partial,
                int max_splits, hipStream_t s);
+int dgemm_splits(int K);   // K-slices dgemm_bf16 uses (K / 128)
 int dgemm_f32(const float* x, const float* w, int D, int N, int K, float* partial,
               int max_splits, hipStream_t s);
 // out = epilogue(sum_s partial[s] + bias): mode 0 store (T), 1 gelu (T), 2 residual add (f32).
 template <typename T>
 void dgemm_reduce(const float* partial, int splits, int D, int N, const float* bias, int mode,
                   void* out, hipStream_t s);
+
+// h[b] += bias + sum_s partial[s][b]; xn[b] = LayerNorm(h[b]) with (g, beta).  d <= 2048.
+template <typename T>
+void reduce_resid_ln(const float* partial, int splits, int D, int d, const float* bias, float* h,
+                     const float* g, const float* beta, T* xn, hipStream_t s);
 
 // Vocabulary projection fused with argmax: keys[b][tile] (ordered value, lowest index).
 void vocab_argmax_bf16(const bf16_t* x, const bf16_t* emb, int D, int V, int K,

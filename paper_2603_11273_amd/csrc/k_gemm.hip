@@ -60,28 +60,119 @@ __device__ __forceinline__ void epi_apply(const Epilogue& e, int r, int n, float
   }
 }
 
-// Epilogue of one 32x32 accumulator block staged in LDS (row stride 33).  V
-// blocks of the fused QKV product are walked column-major so that lanes run
-// along positions, the contiguous direction of the transposed V.
+// Four consecutive columns n..n+3 of row r (n % 4 == 0), bias not yet added.
+__device__ __forceinline__ void st4_bf16(bf16_t* p, float4 v) {
+  uint2 u;
+  u.x = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
+  u.y = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
+  *(uint2*)p = u;
+}
+__device__ __forceinline__ float4 gelu4(float4 v) {
+  return make_float4(gelu_erf(v.x), gelu_erf(v.y), gelu_erf(v.z), gelu_erf(v.w));
+}
+__device__ __forceinline__ float4 add4(float4 a, float4 b) {
+  return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+}
+
 template <int KIND>
-__device__ __forceinline__ void epi_block(const Epilogue& e, const float* stage, int rbase,
-                                          int cbase, int M, int N, int lane) {
-  const int l32 = lane & 31, lh = lane >> 5;
-  if (KIND == EPI_QKV && cbase >= 2 * e.d_model) {
-#pragma unroll 2
-    for (int t = 0; t < 16; ++t) {
-      const int cc = t * 2 + lh;
-      const int row = rbase + l32, col = cbase + cc;
-      if (row < M && col < N) epi_apply<KIND, bf16_t>(e, row, col, stage[l32 * 33 + cc]);
-    }
-  } else {
-#pragma unroll 2
-    for (int t = 0; t < 16; ++t) {
-      const int rr = t * 2 + lh;
-      const int row = rbase + rr, col = cbase + l32;
-      if (row < M && col < N) epi_apply<KIND, bf16_t>(e, row, col, stage[rr * 33 + l32]);
-    }
+__device__ __forceinline__ void epi_apply4(const Epilogue& e, int r, int n, float4 v) {
+  if (e.bias) v = add4(v, *(const float4*)(e.bias + n));
+  if constexpr (KIND == EPI_STORE || KIND == EPI_QKV) {
+    st4_bf16((bf16_t*)e.out + (int64_t)r * e.ldc + n, v);
+  } else if constexpr (KIND == EPI_GELU) {
+    st4_bf16((bf16_t*)e.out + (int64_t)r * e.ldc + n, gelu4(v));
+  } else if constexpr (KIND == EPI_RESID) {
+    float4* x = (float4*)((float*)e.out + (int64_t)r * e.ldc + n);
+    *x = add4(*x, v);
+  } else if constexpr (KIND == EPI_CONV1) {
+    const int g = r / kFrames, t = r - g * kFrames;
+    const int64_t base = (int64_t)g * (kFrames + 1) * e.d_model;
+    st4_bf16((bf16_t*)e.out + base + (int64_t)(t + 1) * e.d_model + n, gelu4(v));
+    if (t == 0) st4_bf16((bf16_t*)e.out + base + n, make_float4(0.f, 0.f, 0.f, 0.f));
+  } else if constexpr (KIND == EPI_CONV2) {
+    const int t = r % kCtx;
+    *(float4*)((float*)e.out + (int64_t)r * e.ldc + n) =
+        add4(gelu4(v), *(const float4*)(e.pos + (int64_t)t * e.ldc + n));
+  } else if constexpr (KIND == EPI_XKV) {
+    const int g = r / kCtx, t = r - g * kCtx;
+    const int two_d = 2 * e.d_model;
+    const int l = n / two_d, rem = n - l * two_d;
+    const int kv = rem >= e.d_model, hd = rem - kv * e.d_model;
+    const int64_t addr = (int64_t)e.slots[g] * e.slot_stride +
+                         ((((int64_t)l * 2 + kv) * e.n_head + (hd >> 6)) * kCtx + t) * kHeadDim +
+                         (hd & 63);
+    st4_bf16((bf16_t*)e.out + addr, v);
   }
+}
+
+// Epilogue of a wave's FM x FN accumulator blocks.  Each 32x32 block goes
+// through the wave's private LDS stage (row stride 36 floats) in the MFMA
+// output layout -- lane holds column lane%32 and, for register r, row
+// 8*(r/4) + 4*(lane/32) + r%4 -- and is read back as four consecutive
+// columns of one row per lane, so every store moves 8 or 16 bytes.  Blocks of
+// the transposed V of the fused QKV product are read back as four
+// consecutive rows of one column instead (contiguous in V^T).  The stage is
+// private to the wave and LDS executes a wave's accesses in order, so no
+// barrier is needed between blocks; the caller synchronises the block once
+// before the first block (the stage aliases the operand ring).
+constexpr int kStageLd = 36;
+
+template <int KIND, int FM, int FN>
+__device__ __forceinline__ void epi_wave(const Epilogue& e, f32x16 (&acc)[FM][FN], float* stage,
+                                         int m0w, int n0w, int M, int N, int lane) {
+  const int l32 = lane & 31, lh = lane >> 5;
+  const bool vec_ok = (N & 3) == 0 && (e.ldc & 3) == 0 && (e.d_model & 3) == 0;
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        stage[((r >> 2) * 8 + lh * 4 + (r & 3)) * kStageLd + l32] = acc[i][j][r];
+      __builtin_amdgcn_wave_barrier();
+      const int rbase = m0w + i * 32, cbase = n0w + j * 32;
+      if (KIND == EPI_QKV && cbase >= 2 * e.d_model) {
+        // V columns: lane takes rows 4q..4q+3 of one column
+        const int r4 = (lane & 7) * 4;
+#pragma unroll 1
+        for (int it = 0; it < 4; ++it) {
+          const int c = it * 8 + (lane >> 3), n = cbase + c;
+          if (n >= N) continue;
+          const int row = rbase + r4;
+          float4 v = make_float4(stage[r4 * kStageLd + c], stage[(r4 + 1) * kStageLd + c],
+                                 stage[(r4 + 2) * kStageLd + c], stage[(r4 + 3) * kStageLd + c]);
+          if (row + 3 < M) {
+            const float b = e.bias ? e.bias[n] : 0.f;
+            v = add4(v, make_float4(b, b, b, b));
+            const int g = row / kCtx, t = row - g * kCtx;    // t % 4 == 0: same clip
+            const int hd = n - 2 * e.d_model;
+            const int64_t addr =
+                (((int64_t)g * e.n_head + (hd >> 6)) * kHeadDim + (hd & 63)) * kVtLd + t;
+            st4_bf16((bf16_t*)e.out2 + addr, v);
+          } else {
+            const float vv[4] = {v.x, v.y, v.z, v.w};
+            for (int q = 0; q < 4; ++q)
+              if (row + q < M) epi_apply<KIND, bf16_t>(e, row + q, n, vv[q]);
+          }
+        }
+      } else {
+        const int c4 = (lane & 7) * 4;
+#pragma unroll 1
+        for (int it = 0; it < 4; ++it) {
+          const int rr = it * 8 + (lane >> 3), row = rbase + rr, n = cbase + c4;
+          if (row >= M || n >= N) continue;
+          const float4 v = *(const float4*)&stage[rr * kStageLd + c4];
+          if (vec_ok) {
+            epi_apply4<KIND>(e, row, n, v);
+          } else {
+            const float vv[4] = {v.x, v.y, v.z, v.w};
+            for (int q = 0; q < 4; ++q)
+              if (n + q < N) epi_apply<KIND, bf16_t>(e, row, n + q, vv[q]);
+          }
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
 }
 
 __device__ __forceinline__ int64_t arow_offset(const AView& a, int r) {
@@ -258,18 +349,8 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(AView a, const bf16_t
   // and read back as two full rows per instruction, so the (possibly heavy)
   // epilogue math runs in a short rolled loop and every store covers whole
   // 32-column row segments.
-  float* stage = (float*)smem + wave * (32 * 33);
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        stage[((r >> 2) * 8 + (lane >> 5) * 4 + (r & 3)) * 33 + lrow] = acc[i][j][r];
-      __syncthreads();
-      epi_block<KIND>(e, stage, m0 + wm * TM + i * 32, n0 + wn * TN + j * 32, M, N, lane);
-      __syncthreads();
-    }
+  epi_wave<KIND, FM, FN>(e, acc, (float*)smem + wave * (32 * kStageLd), m0 + wm * TM,
+                         n0 + wn * TN, M, N, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -307,7 +388,7 @@ __device__ __forceinline__ void lds_dma16(uint32_t lds_addr, const void* gptr) {
                :: "s"(lds_addr), "v"(gptr) : "memory", "m0");
 }
 
-template <int BM, int BN, int BK, int WM, int WN, int S, int KIND>
+template <int BM, int BN, int BK, int WM, int WN, int S, int KIND, int SCHED = 0>
 __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16_dma(AView a,
                                                               const bf16_t* __restrict__ w,
                                                               int M, int N, int K, Epilogue e,
@@ -413,32 +494,198 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16_dma(AView a,
 #pragma unroll
         for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[p][i], bfr[p][j], acc[i][j], 0, 0, 0);
+      if constexpr (SCHED == 1) {
+        // interleave the next step's fragment reads with this step's MFMAs
+        if (kk + 1 < BK / 16) {
+#pragma unroll
+          for (int q = 0; q < FM + FN; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+          __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - (FM + FN), 0);
+        }
+      }
     }
   }
   wait_vmcnt<0>();
   __syncthreads();
 
-  float* stage = (float*)smem + wave * (32 * 33);
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        stage[((r >> 2) * 8 + (lane >> 5) * 4 + (r & 3)) * 33 + lrow] = acc[i][j][r];
-      __syncthreads();
-      epi_block<KIND>(e, stage, m0 + wm * TM + i * 32, n0 + wn * TN + j * 32, M, N, lane);
-      __syncthreads();
-    }
+  epi_wave<KIND, FM, FN>(e, acc, (float*)smem + wave * (32 * kStageLd), m0 + wm * TM,
+                         n0 + wn * TN, M, N, lane);
+}
+
+// Same operand ring, with the fragment reads software-pipelined across K
+// tiles: the barrier that publishes tile kt+1 sits before the MFMAs of the
+// last k-step of tile kt, so the first fragments of tile kt+1 are read while
+// those MFMAs run, and no k-step ever waits on a fragment read issued just
+// before it.  All S stages are in flight: tile kt+S is requested as soon as
+// every wave has finished reading tile kt.  sched_barrier fences keep the
+// compiler from sinking the prefetching reads below the MFMAs.
+template <int VM>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4));
+}
+template <int MAXN>
+__device__ __forceinline__ void wait_vm_lgkm0_rt(int n) {
+  if constexpr (MAXN > 0) {
+    if (n >= MAXN) { wait_vm_lgkm0<MAXN>(); return; }
+    wait_vm_lgkm0_rt<MAXN - 1>(n);
+  } else {
+    wait_vm_lgkm0<0>();
+  }
 }
 
 template <int BM, int BN, int BK, int WM, int WN, int S, int KIND>
+__global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16_pf(AView a,
+                                                             const bf16_t* __restrict__ w,
+                                                             int M, int N, int K, Epilogue e,
+                                                             int n_tm, int n_tn, int gm) {
+  constexpr int NW = WM * WN;
+  constexpr int TM = BM / WM, TN = BN / WN;
+  constexpr int FM = TM / 32, FN = TN / 32;
+  constexpr int CPR = BK / 8;
+  constexpr int NS = BK / 16;                      // MFMA k-steps per tile
+  constexpr int RPI = 1024 / (BK * 2);
+  constexpr int IA = BM / (RPI * NW), IB = BN / (RPI * NW);
+  constexpr int LPT = IA + IB;
+  static_assert(BK == 32 || BK == 64, "BK");
+  static_assert(IA * RPI * NW == BM && IB * RPI * NW == BN, "tile/waves");
+  static_assert(S >= 2 && LPT * (S - 1) < 64, "stages");
+  extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
+  constexpr int STAGE = (BM + BN) * BK;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % WM, wn = wave / WM;
+  int tm, tn;
+  tile_of(blockIdx.x, n_tm * n_tn, n_tm, n_tn, gm, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const uint32_t lds0 =
+      (uint32_t)(uintptr_t)((__attribute__((address_space(3))) bf16_t*)smem);
+
+  const bf16_t* abase = (const bf16_t*)a.ptr;
+  const bf16_t* asrc[IA];
+  uint32_t adst[IA];
+#pragma unroll
+  for (int i = 0; i < IA; ++i) {
+    const int r0 = (i * NW + wave) * RPI;
+    const int row = r0 + lane / CPR;
+    const int c = (lane % CPR) ^ lds_swz<BK>(row);
+    const int r = min(m0 + row, M - 1);
+    const int g = r / a.rows_per_batch;
+    asrc[i] = abase + (int64_t)g * a.batch_stride + (int64_t)(r - g * a.rows_per_batch) * a.lda +
+              c * 8;
+    adst[i] = __builtin_amdgcn_readfirstlane(lds0 + (uint32_t)(r0 * BK * 2));
+  }
+  const bf16_t* bsrc[IB];
+  uint32_t bdst[IB];
+#pragma unroll
+  for (int i = 0; i < IB; ++i) {
+    const int r0 = (i * NW + wave) * RPI;
+    const int row = r0 + lane / CPR;
+    const int c = (lane % CPR) ^ lds_swz<BK>(row);
+    bsrc[i] = w + (int64_t)min(n0 + row, N - 1) * K + c * 8;
+    bdst[i] = __builtin_amdgcn_readfirstlane(lds0 + (uint32_t)((BM * BK + r0 * BK) * 2));
+  }
+  const int nk = K / BK;
+  auto issue = [&](int tile) {
+    const uint32_t so = (uint32_t)((tile % S) * STAGE * 2);
+    const int k0 = tile * BK;
+#pragma unroll
+    for (int i = 0; i < IA; ++i) lds_dma16(adst[i] + so, asrc[i] + k0);
+#pragma unroll
+    for (int i = 0; i < IB; ++i) lds_dma16(bdst[i] + so, bsrc[i] + k0);
+  };
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int lrow = lane & 31, sw = lds_swz<BK>(lrow), lh = lane >> 5;
+  const bf16_t* a_frag = smem + (wm * TM + lrow) * BK;
+  const bf16_t* b_frag = smem + BM * BK + (wn * TN + lrow) * BK;
+  bf16x8 af[2][FM], bfr[2][FN];
+#define PF_READ(P, TILE, KK)                                                          \
+  do {                                                                                \
+    const int off_ = ((TILE) % S) * STAGE + ((((KK) * 2 + lh) ^ sw) * 8);             \
+    _Pragma("unroll") for (int i = 0; i < FM; ++i)                                    \
+      af[P][i] = *(const bf16x8*)(a_frag + off_ + i * 32 * BK);                       \
+    _Pragma("unroll") for (int j = 0; j < FN; ++j)                                    \
+      bfr[P][j] = *(const bf16x8*)(b_frag + off_ + j * 32 * BK);                      \
+  } while (0)
+
+  // Issued right after a fragment prefetch, this tells the wait-count pass
+  // that every older LDS read has completed (the reads feeding the coming
+  // MFMAs), which it cannot prove by itself across the loop back edge.
+  constexpr int kLgkmImm = 0xF | (0x3 << 14) | (0x7 << 4) | ((FM + FN) << 8);
+  static_assert(FM + FN <= 15, "lgkmcnt");
+
+#pragma unroll
+  for (int t = 0; t < S; ++t)
+    if (t < nk) issue(t);
+  wait_vm_lgkm0_rt<LPT*(S - 1)>(LPT * min(S - 1, nk - 1));
+  __builtin_amdgcn_s_barrier();
+  PF_READ(0, 0, 0);
+  for (int kt = 0; kt < nk; ++kt) {
+#pragma unroll
+    for (int kk = 0; kk < NS; ++kk) {
+      const int p = kk & 1;
+      if (kk + 1 < NS) {
+        PF_READ(p ^ 1, kt, kk + 1);
+      } else if (kt + 1 < nk) {
+        // tile kt+1 landed (later tiles may still fly), this wave's reads of
+        // tile kt done; after the barrier nobody reads tile kt any more
+        wait_vm_lgkm0_rt<LPT*(S - 2)>(LPT * min(S - 2, nk - 2 - kt));
+        __builtin_amdgcn_s_barrier();
+        if (kt + S < nk) issue(kt + S);
+        PF_READ(p ^ 1, kt + 1, 0);
+      }
+      if (kk + 1 < NS || kt + 1 < nk) __builtin_amdgcn_s_waitcnt(kLgkmImm);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[p][i], bfr[p][j], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+#undef PF_READ
+  wait_vmcnt<0>();
+  __syncthreads();
+
+  epi_wave<KIND, FM, FN>(e, acc, (float*)smem + wave * (32 * kStageLd), m0 + wm * TM,
+                         n0 + wn * TN, M, N, lane);
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int S, int KIND>
+static void launch_gemm_pf(const AView& a, const bf16_t* w, int M, int N, int K,
+                           const Epilogue& e, hipStream_t s, int gm) {
+  constexpr size_t lds0 = (size_t)S * (BM + BN) * BK * sizeof(bf16_t);
+  constexpr size_t lds_epi = (size_t)WM * WN * 32 * kStageLd * sizeof(float);
+  constexpr size_t lds = lds0 > lds_epi ? lds0 : lds_epi;
+  auto kfn = k_gemm_bf16_pf<BM, BN, BK, WM, WN, S, KIND>;
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)lds);
+    attr = true;
+  }
+  int n_tm = (M + BM - 1) / BM, n_tn = (N + BN - 1) / BN;
+  kfn<<<n_tm * n_tn, WM * WN * 64, lds, s>>>(a, w, M, N, K, e, n_tm, n_tn, gm);
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int S, int KIND, int SCHED = 0>
 static void launch_gemm_dma(const AView& a, const bf16_t* w, int M, int N, int K,
                             const Epilogue& e, hipStream_t s, int gm) {
   constexpr size_t lds0 = (size_t)S * (BM + BN) * BK * sizeof(bf16_t);
-  constexpr size_t lds_epi = (size_t)WM * WN * 32 * 33 * sizeof(float);
+  constexpr size_t lds_epi = (size_t)WM * WN * 32 * kStageLd * sizeof(float);
   constexpr size_t lds = lds0 > lds_epi ? lds0 : lds_epi;
-  auto kfn = k_gemm_bf16_dma<BM, BN, BK, WM, WN, S, KIND>;
+  auto kfn = k_gemm_bf16_dma<BM, BN, BK, WM, WN, S, KIND, SCHED>;
   static bool attr = false;
   if (!attr) {
     (void)hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -453,7 +700,7 @@ template <int BM, int BN, int BK, int WM, int WN, int KIND>
 static void launch_gemm_cfg(const AView& a, const bf16_t* w, int M, int N, int K,
                             const Epilogue& e, hipStream_t s, int gm) {
   constexpr size_t lds0 = (size_t)2 * (BM + BN) * BK * sizeof(bf16_t);
-  constexpr size_t lds_epi = (size_t)WM * WN * 32 * 33 * sizeof(float);
+  constexpr size_t lds_epi = (size_t)WM * WN * 32 * kStageLd * sizeof(float);
   constexpr size_t lds = lds0 > lds_epi ? lds0 : lds_epi;
   auto kfn = k_gemm_bf16<BM, BN, BK, WM, WN, KIND>;
   static bool attr = false;
@@ -467,11 +714,12 @@ static void launch_gemm_cfg(const AView& a, const bf16_t* w, int M, int N, int K
 }
 
 // Tile choice by shape (measured on MI355X with the encoder's products):
-// deep-K products (K >= 2048) use 256x256x64 tiles, two LDS stages, 8 waves of
-// 128x64; the rest 256x128x32 with three stages, 8 waves of 64x64; small
-// products 128x128x32 with four stages so that enough workgroups exist.  K not
-// a multiple of 32 (the 80-mel first convolution) takes the register-path
-// kernel, which zero-fills the K tail.
+// 256x256x64 tiles, two LDS stages, 8 waves of 128x64, fragment reads
+// pipelined across K tiles, wherever K is a multiple of 64 and at least 512
+// tiles exist; otherwise 256x128x32 with three stages (8 waves of 64x64), and
+// 128x128x32 with four stages when even those tiles would be too few to fill
+// the chip.  K not a multiple of 32 (the 80-mel first convolution) takes the
+// register-path kernel, which zero-fills the K tail.
 template <int KIND>
 static void launch_gemm_bf16(const AView& a, const bf16_t* w, int M, int N, int K,
                              const Epilogue& e, hipStream_t s) {
@@ -482,10 +730,10 @@ static void launch_gemm_bf16(const AView& a, const bf16_t* w, int M, int N, int 
       launch_gemm_cfg<256, 128, 32, 4, 2, KIND>(a, w, M, N, K, e, s, 4);
     else
       launch_gemm_cfg<128, 128, 32, 2, 2, KIND>(a, w, M, N, K, e, s, 8);
-  } else if (K >= 2048 && K % 64 == 0 && t256x256 >= 512) {
-    launch_gemm_dma<256, 256, 64, 2, 4, 2, KIND>(a, w, M, N, K, e, s, 4);
+  } else if (K % 64 == 0 && t256x256 >= 512) {
+    launch_gemm_pf<256, 256, 64, 2, 4, 2, KIND>(a, w, M, N, K, e, s, 4);
   } else if (t256x128 >= 512) {
-    launch_gemm_dma<256, 128, 32, 4, 2, 3, KIND>(a, w, M, N, K, e, s, 4);
+    launch_gemm_pf<256, 128, 32, 4, 2, 3, KIND>(a, w, M, N, K, e, s, 4);
   } else {
     launch_gemm_dma<128, 128, 32, 2, 2, 4, KIND>(a, w, M, N, K, e, s, 8);
   }
@@ -576,62 +824,87 @@ void gemm_f32(const AView& a, const float* w, int M, int N, int K, const Epilogu
 // ---------------------------------------------------------------------------
 // Decode GEMMs
 // ---------------------------------------------------------------------------
-// One block: 64 output columns x all decode rows (one wave per 32 rows) over
-// one K-split.  The weight rows are the MFMA "A" operand, the activation rows
-// the "B" operand, so each lane ends with one row's values for 16 columns.
+// One block: 128 output columns (one wave per 32) x all decode rows (up to
+// 128) over one 128-deep K slice.  Every global load of the block is issued
+// up front: the activation slice [128][128] goes to LDS (shared by the four
+// waves), each wave's 32 weight rows x 128 go straight to registers in MFMA
+// operand layout.  The weight rows are the MFMA "A" operand and are read from
+// memory exactly once; partial sums of each K slice go to `partial`.
+constexpr int DG_KC = 128;
+
 __global__ __launch_bounds__(256) void k_dgemm_bf16(const bf16_t* __restrict__ x,
                                                     const bf16_t* __restrict__ w, int D, int N,
-                                                    int K, int kc, float* partial) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int n0 = blockIdx.x * 64, split = blockIdx.y;
-  const int kb = split * kc, ke = min(K, kb + kc);
-  const int b0 = wave * 32;
-  if (b0 >= D) return;
-  const int brow = b0 + (lane & 31);
-  const int lk = (lane >> 5) * 8;
-  const bf16_t* xp = x + (int64_t)min(brow, D - 1) * K + lk;
-  const bf16_t* wp0 = w + (int64_t)min(n0 + (lane & 31), N - 1) * K + lk;
-  const bf16_t* wp1 = w + (int64_t)min(n0 + 32 + (lane & 31), N - 1) * K + lk;
-  f32x16 acc0, acc1;
+                                                    int K, float* partial) {
+  __shared__ __attribute__((aligned(16))) bf16_t Xs[128 * DG_KC];   // [row][k], swizzled chunks
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n0 = blockIdx.x * 128 + wave * 32, split = blockIdx.y;
+  const int k0 = split * DG_KC;
+  const int l32 = lane & 31, lh = lane >> 5;
+  // activation slice: 128 rows x 16 chunks of 16 bytes, 8 chunks per thread
+  uint4 xr[8];
 #pragma unroll
-  for (int r = 0; r < 16; ++r) acc0[r] = acc1[r] = 0.f;
-#pragma unroll 4
-  for (int k = kb; k < ke; k += 16) {
-    bf16x8 xb = *(const bf16x8*)(xp + k);
-    bf16x8 w0 = *(const bf16x8*)(wp0 + k);
-    bf16x8 w1 = *(const bf16x8*)(wp1 + k);
-    acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w0, xb, acc0, 0, 0, 0);
-    acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w1, xb, acc1, 0, 0, 0);
+  for (int i = 0; i < 8; ++i) {
+    const int c = tid + i * 256, row = c >> 4, ch = c & 15;
+    xr[i] = *(const uint4*)(x + (int64_t)min(row, D - 1) * K + k0 + ch * 8);
   }
-  if (brow >= D) return;
-  float* out = partial + ((int64_t)split * D + brow) * N;
+  // weight fragments: row n0 + lane%32, k = k0 + 16 s + 8 (lane/32)
+  bf16x8 wf[DG_KC / 16];
+  const bf16_t* wp = w + (int64_t)min(n0 + l32, N - 1) * K + k0 + lh * 8;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    int n = n0 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-    if (n < N) out[n] = acc0[r];
-    if (n + 32 < N) out[n + 32] = acc1[r];
+  for (int s2 = 0; s2 < DG_KC / 16; ++s2) wf[s2] = *(const bf16x8*)(wp + s2 * 16);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int c = tid + i * 256, row = c >> 4, ch = c & 15;
+    *(uint4*)&Xs[row * DG_KC + ((ch ^ (row & 15)) * 8)] = xr[i];
+  }
+  __syncthreads();
+  if (n0 >= N) return;
+  const int nb = (D + 31) / 32;
+  f32x16 acc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
+#pragma unroll
+  for (int s2 = 0; s2 < DG_KC / 16; ++s2) {
+    const int ch = s2 * 2 + lh;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (j < nb) {
+        const int row = j * 32 + l32;
+        const bf16x8 xf = *(const bf16x8*)&Xs[row * DG_KC + ((ch ^ (row & 15)) * 8)];
+        acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[s2], xf, acc[j], 0, 0, 0);
+      }
+  }
+  // lane holds decode row j*32 + lane%32 and columns n0 + 8(r/4) + 4(lane/32) + r%4
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int brow = j * 32 + l32;
+    if (j >= nb || brow >= D) continue;
+    float* out = partial + ((int64_t)split * D + brow) * N;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int n = n0 + g * 8 + lh * 4;
+      if ((N & 3) == 0 && n + 3 < N) {
+        *(float4*)(out + n) = make_float4(acc[j][g * 4], acc[j][g * 4 + 1], acc[j][g * 4 + 2],
+                                          acc[j][g * 4 + 3]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (n + i < N) out[n + i] = acc[j][g * 4 + i];
+      }
+    }
   }
 }
 
-static int choose_kc(int N, int K, int max_splits) {
-  // aim for >= ~512 workgroups while keeping each split >= 128 deep
-  int n_tiles = (N + 63) / 64;
-  int splits = (512 + n_tiles - 1) / n_tiles;
-  int max_by_depth = K / 128 > 0 ? K / 128 : 1;
-  if (splits > max_by_depth) splits = max_by_depth;
-  if (splits > max_splits) splits = max_splits;
-  if (splits < 1) splits = 1;
-  int kc = (K + splits - 1) / splits;
-  kc = (kc + 15) / 16 * 16;
-  return kc;
-}
+int dgemm_splits(int K) { return K / DG_KC; }
 
 int dgemm_bf16(const bf16_t* x, const bf16_t* w, int D, int N, int K, float* partial,
                int max_splits, hipStream_t s) {
-  int kc = choose_kc(N, K, max_splits);
-  int splits = (K + kc - 1) / kc;
-  dim3 grid((N + 63) / 64, splits);
-  if (D > 0) k_dgemm_bf16<<<grid, 256, 0, s>>>(x, w, D, N, K, kc, partial);
+  const int splits = K / DG_KC;                     // K is a multiple of 128 (checked at create)
+  if (splits > max_splits || D <= 0) return splits;
+  dim3 grid((N + 127) / 128, splits);
+  k_dgemm_bf16<<<grid, 256, 0, s>>>(x, w, D, N, K, partial);
   return splits;
 }
 
@@ -679,10 +952,74 @@ template void dgemm_reduce<float>(const float*, int, int, int, const float*, int
 template void dgemm_reduce<bf16_t>(const float*, int, int, int, const float*, int, void*,
                                    hipStream_t);
 
+// Split-K reduce fused with the residual add and the next LayerNorm: one
+// block per decode row; the row (d <= 2048) stays in registers, 4 values per
+// thread:  h[b] += bias + sum_s partial[s][b];  xn[b] = LN(h[b]) (eps 1e-5).
+template <typename T>
+__global__ __launch_bounds__(512) void k_reduce_resid_ln(const float* __restrict__ partial,
+                                                         int splits, int D, int d,
+                                                         const float* __restrict__ bias,
+                                                         float* __restrict__ h,
+                                                         const float* __restrict__ g,
+                                                         const float* __restrict__ beta, T* xn) {
+  __shared__ float red[2][8];
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nw = blockDim.x >> 6;
+  float v[4];
+  float sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int n = tid + i * blockDim.x;
+    v[i] = 0.f;
+    if (n < d) {
+      float a = h[(int64_t)b * d + n] + bias[n];
+      for (int s = 0; s < splits; ++s) a += partial[((int64_t)s * D + b) * d + n];
+      h[(int64_t)b * d + n] = a;
+      v[i] = a;
+      sum += a;
+    }
+  }
+  sum = wave_sum(sum);
+  if (lane == 0) red[0][wave] = sum;
+  __syncthreads();
+  float tot = 0.f;
+  for (int w2 = 0; w2 < nw; ++w2) tot += red[0][w2];
+  const float mean = tot / d;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int n = tid + i * blockDim.x;
+    if (n < d) q += (v[i] - mean) * (v[i] - mean);
+  }
+  q = wave_sum(q);
+  if (lane == 0) red[1][wave] = q;
+  __syncthreads();
+  float var = 0.f;
+  for (int w2 = 0; w2 < nw; ++w2) var += red[1][w2];
+  const float rstd = rsqrtf(var / d + 1e-5f);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int n = tid + i * blockDim.x;
+    if (n < d) St<T>::st(xn, (int64_t)b * d + n, (v[i] - mean) * rstd * g[n] + beta[n]);
+  }
+}
+
+template <typename T>
+void reduce_resid_ln(const float* partial, int splits, int D, int d, const float* bias, float* h,
+                     const float* g, const float* beta, T* xn, hipStream_t s) {
+  if (D <= 0) return;
+  int threads = ((d + 3) / 4 + 63) / 64 * 64;      // 4 values per thread, whole waves
+  k_reduce_resid_ln<T><<<D, threads, 0, s>>>(partial, splits, D, d, bias, h, g, beta, xn);
+}
+template void reduce_resid_ln<float>(const float*, int, int, int, const float*, float*,
+                                     const float*, const float*, float*, hipStream_t);
+template void reduce_resid_ln<bf16_t>(const float*, int, int, int, const float*, float*,
+                                      const float*, const float*, bf16_t*, hipStream_t);
+
 // ---------------------------------------------------------------------------
 // Vocabulary projection + argmax
 // ---------------------------------------------------------------------------
-int vocab_tiles(int V) { return (V + 63) / 64; }
+int vocab_tiles(int V) { return (V + 31) / 32; }
 
 // Larger key = larger value, then lower index.  Any NaN gets the largest
 // value key so that it always wins and the finishing pass reports it.
@@ -691,55 +1028,62 @@ __device__ __forceinline__ uint64_t argmax_key(float v, int n) {
   return ((uint64_t)o << 32) | (uint64_t)(0xffffffffu - (uint32_t)n);
 }
 
+// One block: 128 vocabulary rows (one wave per 32) x all decode rows.  Each
+// vocabulary row is read once; each wave leaves, for every decode row, the
+// best key over its 32 vocabulary rows (tile = 32 rows).
 __global__ __launch_bounds__(256) void k_vocab_bf16(const bf16_t* __restrict__ x,
                                                     const bf16_t* __restrict__ emb, int D, int V,
                                                     int K, uint64_t* keys, int n_tiles,
                                                     float* logits) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int n0 = blockIdx.x * 64;
-  const int b0 = wave * 32;
-  if (b0 >= D) return;
-  const int brow = b0 + (lane & 31);
-  const int lk = (lane >> 5) * 8;
-  const bf16_t* xp = x + (int64_t)min(brow, D - 1) * K + lk;
-  const bf16_t* wp0 = emb + (int64_t)min(n0 + (lane & 31), V - 1) * K + lk;
-  const bf16_t* wp1 = emb + (int64_t)min(n0 + 32 + (lane & 31), V - 1) * K + lk;
-  f32x16 acc0, acc1;
+  const int tile = blockIdx.x * 4 + wave;
+  const int n0 = tile * 32;
+  if (n0 >= V) return;
+  const int lk = (lane >> 5) * 8, l32 = lane & 31;
+  const int nb = (D + 31) / 32;
+  const bf16_t* wp = emb + (int64_t)min(n0 + l32, V - 1) * K + lk;
+  const bf16_t* xp[4];
 #pragma unroll
-  for (int r = 0; r < 16; ++r) acc0[r] = acc1[r] = 0.f;
-#pragma unroll 4
+  for (int j = 0; j < 4; ++j) xp[j] = x + (int64_t)min(j * 32 + l32, D - 1) * K + lk;
+  f32x16 acc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
   for (int k = 0; k < K; k += 16) {
-    bf16x8 xb = *(const bf16x8*)(xp + k);
-    bf16x8 w0 = *(const bf16x8*)(wp0 + k);
-    bf16x8 w1 = *(const bf16x8*)(wp1 + k);
-    acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w0, xb, acc0, 0, 0, 0);
-    acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w1, xb, acc1, 0, 0, 0);
-  }
-  uint64_t best = 0;
+    const bf16x8 wf = *(const bf16x8*)(wp + k);
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    int n = n0 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-    if (n < V) {
-      uint64_t k0 = argmax_key(acc0[r], n);
-      best = k0 > best ? k0 : best;
-      if (logits && brow < D) logits[(int64_t)brow * V + n] = acc0[r];
-    }
-    if (n + 32 < V) {
-      uint64_t k1 = argmax_key(acc1[r], n + 32);
-      best = k1 > best ? k1 : best;
-      if (logits && brow < D) logits[(int64_t)brow * V + n + 32] = acc1[r];
-    }
+    for (int j = 0; j < 4; ++j)
+      if (j < nb) {
+        const bf16x8 xf = *(const bf16x8*)(xp[j] + k);
+        acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf, xf, acc[j], 0, 0, 0);
+      }
   }
-  uint32_t lo = (uint32_t)best, hi = (uint32_t)(best >> 32);
-  uint32_t plo = __shfl_xor(lo, 32, 64), phi = __shfl_xor(hi, 32, 64);
-  uint64_t other = ((uint64_t)phi << 32) | plo;
-  best = other > best ? other : best;
-  if (lane < 32 && brow < D) keys[(int64_t)brow * n_tiles + blockIdx.x] = best;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (j >= nb) continue;
+    const int brow = j * 32 + l32;
+    uint64_t best = 0;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int n = n0 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+      if (n < V) {
+        const uint64_t kk = argmax_key(acc[j][r], n);
+        best = kk > best ? kk : best;
+        if (logits && brow < D) logits[(int64_t)brow * V + n] = acc[j][r];
+      }
+    }
+    const uint32_t plo = __shfl_xor((uint32_t)best, 32, 64);
+    const uint32_t phi = __shfl_xor((uint32_t)(best >> 32), 32, 64);
+    const uint64_t other = ((uint64_t)phi << 32) | plo;
+    best = other > best ? other : best;
+    if (lane < 32 && brow < D) keys[(int64_t)brow * n_tiles + tile] = best;
+  }
 }
 
 void vocab_argmax_bf16(const bf16_t* x, const bf16_t* emb, int D, int V, int K, uint64_t* keys,
                        int n_tiles, float* logits, hipStream_t s) {
-  if (D > 0) k_vocab_bf16<<<n_tiles, 256, 0, s>>>(x, emb, D, V, K, keys, n_tiles, logits);
+  if (D > 0) k_vocab_bf16<<<(n_tiles + 3) / 4, 256, 0, s>>>(x, emb, D, V, K, keys, n_tiles, logits);
 }
 
 void vocab_logits_f32(const float* x, const float* emb, int D, int V, int K, float* logits,
@@ -754,9 +1098,9 @@ void vocab_logits_f32(const float* x, const float* emb, int D, int V, int K, flo
 
 __global__ void k_logits_keys(const float* logits, int D, int V, uint64_t* keys, int n_tiles) {
   int tile = blockIdx.x, b = blockIdx.y;
-  int n = tile * 64 + threadIdx.x;
+  int n = tile * 32 + threadIdx.x;                 // 32-entry tiles, upper lanes idle
   uint64_t best = 0;
-  if (n < V) best = argmax_key(logits[(int64_t)b * V + n], n);
+  if (threadIdx.x < 32 && n < V) best = argmax_key(logits[(int64_t)b * V + n], n);
   for (int o = 32; o > 0; o >>= 1) {
     uint32_t lo = __shfl_xor((uint32_t)best, o, 64), hi = __shfl_xor((uint32_t)(best >> 32), o, 64);
     uint64_t other = ((uint64_t)hi << 32) | lo;

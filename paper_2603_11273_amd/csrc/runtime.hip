@@ -87,7 +87,7 @@ struct Layout {
          d_hid = 0, d_partial = 0, d_logits = 0, d_keys = 0, d_argmax = 0, d_flag = 0;
   size_t wstage = 0;
   int64_t wstage_floats = 0;
-  int max_splits = 8;
+  int max_splits = 1;
   std::vector<PackOp> pack;
   std::vector<std::pair<size_t, size_t>> zero_regions;   // (offset, bytes) zeroed before packing
 };
@@ -114,7 +114,7 @@ struct asr_ctx {
   size_t bytes = 0;
   hipStream_t stream = nullptr;
   // timing
-  bool timing = false;
+  int32_t timing = 0;   // bit mask over asr_kernel_class
   std::vector<hipEvent_t> ev_pool;
   size_t ev_used = 0;
   std::vector<TimedLaunch> pending;
@@ -292,7 +292,14 @@ void plan(asr_ctx* c) {
   L.d_q = b.take(D * d * es);
   L.d_att = b.take(D * d * es);
   L.d_hid = b.take(D * F * es);
-  L.d_partial = b.take((int64_t)L.max_splits * D * Nmax * f4);
+  // split-K partial sums: the bf16 decode GEMM splits K in 128-deep slices
+  L.max_splits = c->cfg.dtype == ASR_BF16 ? std::max(dgemm_splits(F), dgemm_splits(d)) : 1;
+  {
+    int64_t most = std::max<int64_t>((int64_t)dgemm_splits(d) * std::max<int64_t>(3 * d, F),
+                                     (int64_t)dgemm_splits(F) * d);
+    if (c->cfg.dtype != ASR_BF16) most = Nmax;
+    L.d_partial = b.take(std::max<int64_t>(most, Nmax) * D * f4);
+  }
   L.d_logits = b.take(D * (int64_t)std::max(1, g.vocab) * f4);
   L.d_keys = b.take(D * (int64_t)vocab_tiles(std::max(1, g.vocab)) * 8);
   L.d_argmax = b.take(D * 4);
@@ -388,7 +395,7 @@ hipEvent_t next_event(asr_ctx* c) {
 
 template <class F>
 void timed(asr_ctx* c, int cls, double flops, double bytes, F&& f) {
-  if (!c->timing) {
+  if (!(c->timing >> cls & 1)) {
     f();
     return;
   }
@@ -409,7 +416,7 @@ struct PhaseMark {
   int cls;
   hipEvent_t a = nullptr;
   PhaseMark(asr_ctx* c_, int cls_) : c(c_), cls(cls_) {
-    if (c->timing) {
+    if (c->timing >> cls & 1) {
       a = next_event(c);
       if (a) (void)hipEventRecord(a, c->stream);
     }
@@ -645,6 +652,27 @@ void dgemm_any(asr_ctx* c, const T* x, size_t w_off, int D, int N, int K, size_t
   });
 }
 
+// Residual product (N = d) whose split-K reduce also adds the residual into h
+// and writes the next LayerNorm (g, b) of h into xn.
+template <typename T>
+void dgemm_resid_ln(asr_ctx* c, const T* x, size_t w_off, int D, int K, size_t bias_off,
+                    float* h, size_t g_off, size_t b_off, T* xn) {
+  const int d = c->cfg.d_model;
+  float* part = c->at<float>(c->L.d_partial);
+  int splits = 1;
+  double bytes = (double)d * K * c->es + (double)D * K * c->es + (double)D * d * (8 + c->es);
+  timed(c, ASR_K_DGEMM, 2.0 * D * d * K, bytes, [&] {
+    if (c->bf16())
+      splits = dgemm_bf16((const bf16_t*)x, c->at<bf16_t>(w_off), D, d, K, part,
+                          c->L.max_splits, c->stream);
+    else
+      splits = dgemm_f32((const float*)x, c->at<float>(w_off), D, d, K, part,
+                         c->L.max_splits, c->stream);
+    reduce_resid_ln<T>(part, splits, D, d, c->at<float>(bias_off), h, c->at<float>(g_off),
+                       c->at<float>(b_off), xn, c->stream);
+  });
+}
+
 template <typename T>
 asr_status decode_rows(asr_ctx* c, int D, const std::vector<int32_t>& pos_host, bool want_logits) {
   const asr_model_cfg& g = c->cfg;
@@ -667,17 +695,17 @@ asr_status decode_rows(asr_ctx* c, int D, const std::vector<int32_t>& pos_host, 
     embed<T>(c->at<T>(L.tok_emb), c->at<float>(L.pos_emb), c->at<int32_t>(L.d_tokens), pos, D, d,
              h, c->stream);
   });
+  ln_any<T>(c, h, D, L.dec[0].ln1_g, L.dec[0].ln1_b, xn);
   for (int l = 0; l < g.n_dec; ++l) {
     const DecLayer& w = L.dec[l];
-    ln_any<T>(c, h, D, w.ln1_g, w.ln1_b, xn);
+    // xn holds LN_attn(h) here
     dgemm_any<T>(c, xn, w.qkv_w, D, 3 * d, d, w.qkv_b, 0, qkv);
     const int64_t self_off = (int64_t)l * 2 * H * kTextCtx * kHeadDim;
     timed(c, ASR_K_DATTN, 4.0 * self_keys * 64 * H, self_keys * 2 * 64 * H * c->es, [&] {
       decode_self_attn<T>(qkv, self_cache, L.self_stride, self_off, slots, pos, D, H, att,
                           c->stream);
     });
-    dgemm_any<T>(c, att, w.o_w, D, d, d, w.o_b, 2, h);
-    ln_any<T>(c, h, D, w.lnx_g, w.lnx_b, xn);
+    dgemm_resid_ln<T>(c, att, w.o_w, D, d, w.o_b, h, w.lnx_g, w.lnx_b, xn);
     dgemm_any<T>(c, xn, w.xq_w, D, d, d, w.xq_b, 0, q);
     const int64_t cross_off = (int64_t)l * 2 * H * kCtx * kHeadDim;
     timed(c, ASR_K_DATTN, 4.0 * D * H * (double)kCtx * 64, (double)D * H * kCtx * 2 * 64 * c->es,
@@ -685,12 +713,13 @@ asr_status decode_rows(asr_ctx* c, int D, const std::vector<int32_t>& pos_host, 
             decode_cross_attn<T>(q, cross_cache, L.cross_stride, cross_off, slots, D, H, att,
                                  c->stream);
           });
-    dgemm_any<T>(c, att, w.xo_w, D, d, d, w.xo_b, 2, h);
-    ln_any<T>(c, h, D, w.ln2_g, w.ln2_b, xn);
+    dgemm_resid_ln<T>(c, att, w.xo_w, D, d, w.xo_b, h, w.ln2_g, w.ln2_b, xn);
     dgemm_any<T>(c, xn, w.fc1_w, D, F, d, w.fc1_b, 1, hid);
-    dgemm_any<T>(c, hid, w.fc2_w, D, d, F, w.fc2_b, 2, h);
+    // the last residual of the layer also produces the next LayerNorm input
+    const bool last = l + 1 == g.n_dec;
+    dgemm_resid_ln<T>(c, hid, w.fc2_w, D, F, w.fc2_b, h, last ? L.lnf_g : L.dec[l + 1].ln1_g,
+                      last ? L.lnf_b : L.dec[l + 1].ln1_b, xn);
   }
-  ln_any<T>(c, h, D, L.lnf_g, L.lnf_b, xn);
   const int nt = vocab_tiles(V);
   int32_t* flag = c->at<int32_t>(L.d_flag);
   fill_u32((uint32_t*)flag, 0u, 1, c->stream);
@@ -751,7 +780,10 @@ asr_status asr_create(const asr_model_cfg* cfg, int32_t device, asr_ctx** out) {
   if (g.n_mels <= 0 || g.d_model <= 0 || g.n_head <= 0 || g.d_model != 64 * g.n_head)
     return fail(ASR_EINVAL, "d_model must equal 64 * n_head");
   if (g.n_mels % 8 != 0) return fail(ASR_EINVAL, "n_mels must be a multiple of 8");
+  if (g.d_model > 2048) return fail(ASR_EINVAL, "d_model must be <= 2048");
   if (g.d_ffn <= 0 || g.d_ffn % 64 != 0) return fail(ASR_EINVAL, "d_ffn must be a multiple of 64");
+  if (g.dtype == ASR_BF16 && (g.d_model % 128 != 0 || g.d_ffn % 128 != 0))
+    return fail(ASR_EINVAL, "bf16 models need d_model and d_ffn multiples of 128");
   if (g.n_enc < 0 || g.n_dec < 0 || (g.n_enc == 0 && g.n_dec == 0))
     return fail(ASR_EINVAL, "need encoder or decoder layers");
   if (g.n_dec > 0 && g.vocab <= 0) return fail(ASR_EINVAL, "vocab must be positive");
@@ -1065,10 +1097,11 @@ asr_status asr_step(asr_ctx* c, const asr_step_in* in, asr_step_out* out) {
   return collect_timing(c);
 }
 
-asr_status asr_set_timing(asr_ctx* c, int32_t enable) {
+asr_status asr_set_timing(asr_ctx* c, int32_t classes) {
   if (!c) return fail(ASR_EINVAL, "NULL context");
   if (c->device < 0) return fail(ASR_ENODEV, "queue-only context");
-  c->timing = enable != 0;
+  if (classes & ~ASR_TIME_ALL) return fail(ASR_EINVAL, "unknown timing class bits");
+  c->timing = classes;
   return ASR_OK;
 }
 
