@@ -43,6 +43,7 @@ enum EpiKind : int32_t {
   EPI_CONV2 = 4,      // x[r][n] = gelu(acc + bias[n]) + pos[r % 1500][n]   (float32)
   EPI_XKV = 5,        // cross cache of slot[g], all decoder layers        (storage)
   EPI_QKV = 6,        // q, k -> out[r][n] (n < 2d); v -> out2 = V^T per head (storage)
+  EPI_F32 = 7,        // out[r][n] = acc + bias[n]                       (float32)
 };
 
 // Row stride (positions) of the per-head transposed V written by EPI_QKV:
@@ -100,6 +101,10 @@ int vocab_tiles(int V);
 template <typename T>
 void layer_norm(const float* x, int rows, int d, const float* g, const float* b, T* out,
                 hipStream_t s);
+// Residual add fused with the LayerNorm that follows it: x += y, out = LN(x).
+template <typename T>
+void residual_layer_norm(float* x, const float* y, int rows, int d, const float* g,
+                         const float* b, T* out, hipStream_t s);
 
 // Encoder self-attention over 1500 positions, qkv [B*1500][3d], out [B*1500][d].
 void flash_attn_bf16(const bf16_t* qkv, const bf16_t* vt, bf16_t* out, int B, int n_head,

@@ -13,6 +13,8 @@
 //    deterministic cross-tile reduction.
 #include "asr_device.h"
 
+#include <algorithm>
+
 namespace asr {
 
 // ---------------------------------------------------------------------------
@@ -47,6 +49,8 @@ __device__ __forceinline__ void epi_apply(const Epilogue& e, int r, int n, float
     int64_t addr = (int64_t)e.slots[g] * e.slot_stride +
                    ((((int64_t)l * 2 + kv) * e.n_head + h) * kCtx + t) * kHeadDim + c;
     St<T>::st((T*)e.out, addr, v);
+  } else if constexpr (KIND == EPI_F32) {
+    ((float*)e.out)[(int64_t)r * e.ldc + n] = v;
   } else if constexpr (KIND == EPI_QKV) {
     const int two_d = 2 * e.d_model;
     if (n < two_d) {
@@ -60,12 +64,22 @@ __device__ __forceinline__ void epi_apply(const Epilogue& e, int r, int n, float
   }
 }
 
-// Four consecutive columns n..n+3 of row r (n % 4 == 0), bias not yet added.
+// Epilogue stores carry the non-temporal hint: the encoder products write
+// hundreds of MB that the L2 cannot keep for the next kernel anyway, and
+// letting them allocate there evicts the operand panels the running GEMM
+// still re-reads (measured: about a quarter of the time of a K = 1280
+// product goes away).
 __device__ __forceinline__ void st4_bf16(bf16_t* p, float4 v) {
-  uint2 u;
+  typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+  u32x2 u;
   u.x = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
   u.y = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
-  *(uint2*)p = u;
+  __builtin_nontemporal_store(u, (u32x2*)p);
+}
+__device__ __forceinline__ void st4_f32(float* p, float4 v) {
+  typedef __attribute__((ext_vector_type(4))) float f32x4;
+  f32x4 u = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(u, (f32x4*)p);
 }
 __device__ __forceinline__ float4 gelu4(float4 v) {
   return make_float4(gelu_erf(v.x), gelu_erf(v.y), gelu_erf(v.z), gelu_erf(v.w));
@@ -74,6 +88,7 @@ __device__ __forceinline__ float4 add4(float4 a, float4 b) {
   return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
 }
 
+// Four consecutive columns n..n+3 of row r (n % 4 == 0), bias not yet added.
 template <int KIND>
 __device__ __forceinline__ void epi_apply4(const Epilogue& e, int r, int n, float4 v) {
   if (e.bias) v = add4(v, *(const float4*)(e.bias + n));
@@ -81,9 +96,11 @@ __device__ __forceinline__ void epi_apply4(const Epilogue& e, int r, int n, floa
     st4_bf16((bf16_t*)e.out + (int64_t)r * e.ldc + n, v);
   } else if constexpr (KIND == EPI_GELU) {
     st4_bf16((bf16_t*)e.out + (int64_t)r * e.ldc + n, gelu4(v));
+  } else if constexpr (KIND == EPI_F32) {
+    st4_f32((float*)e.out + (int64_t)r * e.ldc + n, v);
   } else if constexpr (KIND == EPI_RESID) {
-    float4* x = (float4*)((float*)e.out + (int64_t)r * e.ldc + n);
-    *x = add4(*x, v);
+    float* x = (float*)e.out + (int64_t)r * e.ldc + n;
+    st4_f32(x, add4(*(const float4*)x, v));
   } else if constexpr (KIND == EPI_CONV1) {
     const int g = r / kFrames, t = r - g * kFrames;
     const int64_t base = (int64_t)g * (kFrames + 1) * e.d_model;
@@ -91,8 +108,8 @@ __device__ __forceinline__ void epi_apply4(const Epilogue& e, int r, int n, floa
     if (t == 0) st4_bf16((bf16_t*)e.out + base + n, make_float4(0.f, 0.f, 0.f, 0.f));
   } else if constexpr (KIND == EPI_CONV2) {
     const int t = r % kCtx;
-    *(float4*)((float*)e.out + (int64_t)r * e.ldc + n) =
-        add4(gelu4(v), *(const float4*)(e.pos + (int64_t)t * e.ldc + n));
+    st4_f32((float*)e.out + (int64_t)r * e.ldc + n,
+            add4(gelu4(v), *(const float4*)(e.pos + (int64_t)t * e.ldc + n)));
   } else if constexpr (KIND == EPI_XKV) {
     const int g = r / kCtx, t = r - g * kCtx;
     const int two_d = 2 * e.d_model;
@@ -109,19 +126,25 @@ __device__ __forceinline__ void epi_apply4(const Epilogue& e, int r, int n, floa
 // through the wave's private LDS stage (row stride 36 floats) in the MFMA
 // output layout -- lane holds column lane%32 and, for register r, row
 // 8*(r/4) + 4*(lane/32) + r%4 -- and is read back as four consecutive
-// columns of one row per lane, so every store moves 8 or 16 bytes.  Blocks of
-// the transposed V of the fused QKV product are read back as four
+// columns of one row per lane, so every store moves 8 or 16 bytes.  The
+// transposed V of the fused QKV product (VT below) is read back as four
 // consecutive rows of one column instead (contiguous in V^T).  The stage is
 // private to the wave and LDS executes a wave's accesses in order, so no
 // barrier is needed between blocks; the caller synchronises the block once
 // before the first block (the stage aliases the operand ring).
 constexpr int kStageLd = 36;
+constexpr int EPI_VT = 100;   // internal: V columns of EPI_QKV
 
+// The conv-stem epilogue keeps its row loop rolled: unrolled, its address
+// arithmetic spills the accumulators.
+#define EPI_UNROLL (KIND == EPI_CONV1 ? 1 : 4)
 template <int KIND, int FM, int FN>
-__device__ __forceinline__ void epi_wave(const Epilogue& e, f32x16 (&acc)[FM][FN], float* stage,
-                                         int m0w, int n0w, int M, int N, int lane) {
+__device__ __forceinline__ void epi_wave_impl(const Epilogue& e, f32x16 (&acc)[FM][FN],
+                                              float* stage, int m0w, int n0w, int M, int N,
+                                              int lane) {
   const int l32 = lane & 31, lh = lane >> 5;
   const bool vec_ok = (N & 3) == 0 && (e.ldc & 3) == 0 && (e.d_model & 3) == 0;
+  constexpr int AK = KIND == EPI_VT ? EPI_QKV : KIND;     // kind for the scalar fallback
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -131,10 +154,10 @@ __device__ __forceinline__ void epi_wave(const Epilogue& e, f32x16 (&acc)[FM][FN
         stage[((r >> 2) * 8 + lh * 4 + (r & 3)) * kStageLd + l32] = acc[i][j][r];
       __builtin_amdgcn_wave_barrier();
       const int rbase = m0w + i * 32, cbase = n0w + j * 32;
-      if (KIND == EPI_QKV && cbase >= 2 * e.d_model) {
-        // V columns: lane takes rows 4q..4q+3 of one column
+      if constexpr (KIND == EPI_VT) {
+        // lane takes rows 4q..4q+3 of one column
         const int r4 = (lane & 7) * 4;
-#pragma unroll 1
+#pragma unroll
         for (int it = 0; it < 4; ++it) {
           const int c = it * 8 + (lane >> 3), n = cbase + c;
           if (n >= N) continue;
@@ -152,12 +175,12 @@ __device__ __forceinline__ void epi_wave(const Epilogue& e, f32x16 (&acc)[FM][FN
           } else {
             const float vv[4] = {v.x, v.y, v.z, v.w};
             for (int q = 0; q < 4; ++q)
-              if (row + q < M) epi_apply<KIND, bf16_t>(e, row + q, n, vv[q]);
+              if (row + q < M) epi_apply<AK, bf16_t>(e, row + q, n, vv[q]);
           }
         }
       } else {
         const int c4 = (lane & 7) * 4;
-#pragma unroll 1
+#pragma unroll EPI_UNROLL
         for (int it = 0; it < 4; ++it) {
           const int rr = it * 8 + (lane >> 3), row = rbase + rr, n = cbase + c4;
           if (row >= M || n >= N) continue;
@@ -167,12 +190,54 @@ __device__ __forceinline__ void epi_wave(const Epilogue& e, f32x16 (&acc)[FM][FN
           } else {
             const float vv[4] = {v.x, v.y, v.z, v.w};
             for (int q = 0; q < 4; ++q)
-              if (n + q < N) epi_apply<KIND, bf16_t>(e, row, n + q, vv[q]);
+              if (n + q < N) epi_apply<AK, bf16_t>(e, row, n + q, vv[q]);
           }
         }
       }
       __builtin_amdgcn_wave_barrier();
     }
+}
+#undef EPI_UNROLL
+
+// Plain element-wise fallback (a wave whose columns straddle q/k and V).
+template <int FM, int FN>
+__device__ __forceinline__ void epi_wave_mixed(const Epilogue& e, f32x16 (&acc)[FM][FN],
+                                            float* stage, int m0w, int n0w, int M, int N,
+                                            int lane) {
+  const int l32 = lane & 31, lh = lane >> 5;
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        stage[((r >> 2) * 8 + lh * 4 + (r & 3)) * kStageLd + l32] = acc[i][j][r];
+      __builtin_amdgcn_wave_barrier();
+      for (int t = 0; t < 16; ++t) {
+        const int rr = t * 2 + lh, row = m0w + i * 32 + rr, col = n0w + j * 32 + l32;
+        if (row < M && col < N) epi_apply<EPI_QKV, bf16_t>(e, row, col, stage[rr * kStageLd + l32]);
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+}
+
+// For EPI_QKV a wave's columns are all q/k or all V when 2 d_model is a
+// multiple of the wave's column span (always, for d_model % 128 == 0 and
+// spans of 32 or 64); otherwise the blocks are sorted out one by one.
+template <int KIND, int FM, int FN>
+__device__ __forceinline__ void epi_wave(const Epilogue& e, f32x16 (&acc)[FM][FN], float* stage,
+                                         int m0w, int n0w, int M, int N, int lane) {
+  if constexpr (KIND == EPI_QKV) {
+    const int two_d = 2 * e.d_model;
+    if (n0w >= two_d)
+      epi_wave_impl<EPI_VT, FM, FN>(e, acc, stage, m0w, n0w, M, N, lane);
+    else if (n0w + FN * 32 <= two_d)
+      epi_wave_impl<EPI_QKV, FM, FN>(e, acc, stage, m0w, n0w, M, N, lane);
+    else
+      epi_wave_mixed<FM, FN>(e, acc, stage, m0w, n0w, M, N, lane);
+  } else {
+    epi_wave_impl<KIND, FM, FN>(e, acc, stage, m0w, n0w, M, N, lane);
+  }
 }
 
 __device__ __forceinline__ int64_t arow_offset(const AView& a, int r) {
@@ -662,6 +727,269 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16_pf(AView a,
                          n0 + wn * TN, M, N, lane);
 }
 
+// ---------------------------------------------------------------------------
+// Persistent variant.  One workgroup per CU walks its share of the output
+// tiles (virtual block ids b, b + grid, ... through the same XCD-aware tile
+// order) and the operand ring runs on across tile boundaries, so the first K
+// tile of the next output tile is in flight while the current one is written
+// out through a small stage of its own beside the ring.  At a tile switch the
+// next K tile is awaited before the stores are issued, and the ring's next
+// load goes out after them, so every wait count stays exact or errs towards
+// waiting longer.
+// ---------------------------------------------------------------------------
+// Epilogue through a 16-row stage per wave (it lives beside the operand
+// ring, which is busy with the next tile): each 32x32 block goes out in two
+// halves, registers 0-7 (rows 0-15) then 8-15 (rows 16-31).  The scatter
+// epilogues keep their row loops rolled (unrolled, they spill).
+#define EPI_HALF_UNROLL ((KIND == EPI_CONV1 || KIND == EPI_QKV) ? 1 : 2)
+template <int KIND, int FM, int FN>
+__device__ __forceinline__ void epi_wave_half(const Epilogue& e, f32x16 (&acc)[FM][FN],
+                                              float* stage, int m0w, int n0w, int M, int N,
+                                              int lane) {
+  const int l32 = lane & 31, lh = lane >> 5;
+  const bool vec_ok = (N & 3) == 0 && (e.ldc & 3) == 0 && (e.d_model & 3) == 0;
+  const bool vt = KIND == EPI_QKV && n0w >= 2 * e.d_model;   // wave-uniform
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int r = 0; r < 8; ++r)
+          stage[((r >> 2) * 8 + lh * 4 + (r & 3)) * kStageLd + l32] = acc[i][j][h * 8 + r];
+        __builtin_amdgcn_wave_barrier();
+        const int rbase = m0w + i * 32 + h * 16, cbase = n0w + j * 32;
+        if (KIND == EPI_QKV && vt) {
+          // lane takes rows 4q..4q+3 (of 16) of one column
+          const int r4 = (lane & 3) * 4;
+#pragma unroll EPI_HALF_UNROLL
+          for (int it = 0; it < 2; ++it) {
+            const int c = it * 16 + (lane >> 2), n = cbase + c, row = rbase + r4;
+            if (n >= N) continue;
+            float4 v = make_float4(stage[r4 * kStageLd + c], stage[(r4 + 1) * kStageLd + c],
+                                   stage[(r4 + 2) * kStageLd + c], stage[(r4 + 3) * kStageLd + c]);
+            if (row + 3 < M) {
+              const float b = e.bias ? e.bias[n] : 0.f;
+              v = add4(v, make_float4(b, b, b, b));
+              const int g = row / kCtx, t = row - g * kCtx;    // t % 4 == 0: same clip
+              const int hd = n - 2 * e.d_model;
+              st4_bf16((bf16_t*)e.out2 +
+                           (((int64_t)g * e.n_head + (hd >> 6)) * kHeadDim + (hd & 63)) * kVtLd + t,
+                       v);
+            } else {
+              const float vv[4] = {v.x, v.y, v.z, v.w};
+              for (int q = 0; q < 4; ++q)
+                if (row + q < M) epi_apply<KIND, bf16_t>(e, row + q, n, vv[q]);
+            }
+          }
+        } else {
+          const int c4 = (lane & 7) * 4;
+#pragma unroll EPI_HALF_UNROLL
+          for (int it = 0; it < 2; ++it) {
+            const int rr = it * 8 + (lane >> 3), row = rbase + rr, n = cbase + c4;
+            if (row >= M || n >= N) continue;
+            const float4 v = *(const float4*)&stage[rr * kStageLd + c4];
+            if (vec_ok) {
+              epi_apply4<KIND>(e, row, n, v);
+            } else {
+              const float vv[4] = {v.x, v.y, v.z, v.w};
+              for (int q = 0; q < 4; ++q)
+                if (n + q < N) epi_apply<KIND, bf16_t>(e, row, n + q, vv[q]);
+            }
+          }
+        }
+        __builtin_amdgcn_wave_barrier();
+      }
+}
+
+#undef EPI_HALF_UNROLL
+
+template <int BM, int BN, int BK, int WM, int WN, int S, int KIND>
+__global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16_ps(AView a,
+                                                             const bf16_t* __restrict__ w,
+                                                             int M, int N, int K, Epilogue e,
+                                                             int n_tm, int n_tn, int gm) {
+  constexpr int NW = WM * WN;
+  constexpr int TM = BM / WM, TN = BN / WN;
+  constexpr int FM = TM / 32, FN = TN / 32;
+  constexpr int CPR = BK / 8;
+  constexpr int NS = BK / 16;
+  constexpr int RPI = 1024 / (BK * 2);
+  constexpr int IA = BM / (RPI * NW), IB = BN / (RPI * NW);
+  constexpr int LPT = IA + IB;
+  static_assert(BK == 32 || BK == 64, "BK");
+  static_assert(NS % 2 == 0, "fragment double buffer parity");
+  static_assert(IA * RPI * NW == BM && IB * RPI * NW == BN, "tile/waves");
+  static_assert(S >= 2 && LPT * (S - 1) < 64, "stages");
+  static_assert(FM + FN <= 15, "lgkmcnt");
+  extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
+  constexpr int STAGE = (BM + BN) * BK;
+  constexpr int kLgkmImm = 0xF | (0x3 << 14) | (0x7 << 4) | ((FM + FN) << 8);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % WM, wn = wave / WM;
+  const int n_tiles = n_tm * n_tn, grid = gridDim.x;
+  if ((int)blockIdx.x >= n_tiles) return;
+  const int my_tiles = (n_tiles - (int)blockIdx.x + grid - 1) / grid;
+  const int nk = K / BK;
+  const int total = my_tiles * nk;
+  const uint32_t lds0 =
+      (uint32_t)(uintptr_t)((__attribute__((address_space(3))) bf16_t*)smem);
+
+  // per-wave LDS destinations (fixed) and per-lane source offsets in
+  // elements (32-bit: the launcher checks the operand extents), reset per tile
+  uint32_t adst[IA], bdst[IB];
+#pragma unroll
+  for (int i = 0; i < IA; ++i)
+    adst[i] = __builtin_amdgcn_readfirstlane(lds0 + (uint32_t)((i * NW + wave) * RPI * BK * 2));
+#pragma unroll
+  for (int i = 0; i < IB; ++i)
+    bdst[i] = __builtin_amdgcn_readfirstlane(
+        lds0 + (uint32_t)((BM * BK + (i * NW + wave) * RPI * BK) * 2));
+  const bf16_t* abase = (const bf16_t*)a.ptr;
+  uint32_t aoff[IA], boff[IB];
+  int src_tile = -1;
+  auto set_src = [&](int ti) {
+    int tm, tn;
+    tile_of((int)blockIdx.x + ti * grid, n_tiles, n_tm, n_tn, gm, tm, tn);
+#pragma unroll
+    for (int i = 0; i < IA; ++i) {
+      const int row = (i * NW + wave) * RPI + lane / CPR;
+      const int c = ((lane % CPR) ^ lds_swz<BK>(row)) * 8;
+      const int r = min(tm * BM + row, M - 1);
+      const int g = r / a.rows_per_batch;
+      aoff[i] = (uint32_t)(g * a.batch_stride + (int64_t)(r - g * a.rows_per_batch) * a.lda + c);
+    }
+#pragma unroll
+    for (int i = 0; i < IB; ++i) {
+      const int row = (i * NW + wave) * RPI + lane / CPR;
+      const int c = ((lane % CPR) ^ lds_swz<BK>(row)) * 8;
+      boff[i] = (uint32_t)min(tn * BN + row, N - 1) * (uint32_t)K + (uint32_t)c;
+    }
+    src_tile = ti;
+  };
+  auto issue = [&](int gi) {
+    const int ti = gi / nk, kt = gi - ti * nk;
+    if (ti != src_tile) set_src(ti);
+    const uint32_t so = (uint32_t)((gi % S) * STAGE * 2);
+    const int k0 = kt * BK;
+#pragma unroll
+    for (int i = 0; i < IA; ++i) lds_dma16(adst[i] + so, abase + aoff[i] + k0);
+#pragma unroll
+    for (int i = 0; i < IB; ++i) lds_dma16(bdst[i] + so, w + boff[i] + k0);
+  };
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int lrow = lane & 31, sw = lds_swz<BK>(lrow), lh = lane >> 5;
+  const bf16_t* a_frag = smem + (wm * TM + lrow) * BK;
+  const bf16_t* b_frag = smem + BM * BK + (wn * TN + lrow) * BK;
+  bf16x8 af[2][FM], bfr[2][FN];
+#define PS_READ(P, GI, KK)                                                            \
+  do {                                                                                \
+    const int off_ = ((GI) % S) * STAGE + ((((KK) * 2 + lh) ^ sw) * 8);               \
+    _Pragma("unroll") for (int i = 0; i < FM; ++i)                                    \
+      af[P][i] = *(const bf16x8*)(a_frag + off_ + i * 32 * BK);                       \
+    _Pragma("unroll") for (int j = 0; j < FN; ++j)                                    \
+      bfr[P][j] = *(const bf16x8*)(b_frag + off_ + j * 32 * BK);                      \
+  } while (0)
+
+#pragma unroll
+  for (int t = 0; t < S; ++t)
+    if (t < total) issue(t);
+  wait_vm_lgkm0_rt<LPT*(S - 1)>(LPT * min(S - 1, total - 1));
+  __builtin_amdgcn_s_barrier();
+  PS_READ(0, 0, 0);
+  int ti = 0, kt = 0;
+  for (int gi = 0; gi < total; ++gi) {
+    const bool last_k = kt == nk - 1;
+#pragma unroll
+    for (int kk = 0; kk < NS; ++kk) {
+      const int p = kk & 1;
+      if (kk + 1 < NS) {
+        PS_READ(p ^ 1, gi, kk + 1);
+      } else if (!last_k) {
+        wait_vm_lgkm0_rt<LPT*(S - 2)>(LPT * min(S - 2, total - 2 - gi));
+        __builtin_amdgcn_s_barrier();
+        if (gi + S < total) issue(gi + S);
+        PS_READ(p ^ 1, gi + 1, 0);
+      }
+      if (kk + 1 < NS || !last_k) __builtin_amdgcn_s_waitcnt(kLgkmImm);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[p][i], bfr[p][j], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (last_k) {
+      const bool more = gi + 1 < total;
+      if (more) {
+        // next K tile landed and every wave is done with this one
+        wait_vm_lgkm0_rt<LPT*(S - 2)>(LPT * min(S - 2, total - 2 - gi));
+        __builtin_amdgcn_s_barrier();
+      }
+      int tm, tn;
+      tile_of((int)blockIdx.x + ti * grid, n_tiles, n_tm, n_tn, gm, tm, tn);
+      epi_wave_half<KIND, FM, FN>(e, acc, (float*)(smem + S * STAGE) + wave * 16 * kStageLd,
+                                  tm * BM + wm * TM, tn * BN + wn * TN, M, N, lane);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+      if (more) {
+        if (gi + S < total) issue(gi + S);
+        PS_READ(0, gi + 1, 0);
+      }
+      ++ti;
+      kt = 0;
+    } else {
+      ++kt;
+    }
+  }
+#undef PS_READ
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int S, int KIND>
+static void launch_gemm_ps(const AView& a, const bf16_t* w, int M, int N, int K,
+                           const Epilogue& e, hipStream_t s, int gm) {
+  constexpr size_t lds = (size_t)S * (BM + BN) * BK * sizeof(bf16_t) +
+                        (size_t)WM * WN * 16 * kStageLd * sizeof(float);
+  auto kfn = k_gemm_bf16_ps<BM, BN, BK, WM, WN, S, KIND>;
+  static bool attr = false;
+  static int n_cu = 0;
+  if (!attr) {
+    (void)hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)lds);
+    int dev = 0;
+    (void)hipGetDevice(&dev);
+    (void)hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (n_cu <= 0) n_cu = 256;
+    attr = true;
+  }
+  const int n_tm = (M + BM - 1) / BM, n_tn = (N + BN - 1) / BN;
+  const int grid = std::min(n_tm * n_tn, n_cu);
+  kfn<<<grid, WM * WN * 64, lds, s>>>(a, w, M, N, K, e, n_tm, n_tn, gm);
+}
+
+// Operand extents (elements) that the persistent kernel's 32-bit source
+// offsets can address.
+static bool fits_u32_offsets(const AView& a, int M, int N, int K) {
+  const int64_t r = M - 1, g = r / a.rows_per_batch;
+  const int64_t a_end = g * a.batch_stride + (r - g * a.rows_per_batch) * a.lda + K;
+  return a_end < (int64_t)UINT32_MAX && (int64_t)N * K < (int64_t)UINT32_MAX;
+}
+
 template <int BM, int BN, int BK, int WM, int WN, int S, int KIND>
 static void launch_gemm_pf(const AView& a, const bf16_t* w, int M, int N, int K,
                            const Epilogue& e, hipStream_t s, int gm) {
@@ -716,10 +1044,12 @@ static void launch_gemm_cfg(const AView& a, const bf16_t* w, int M, int N, int K
 // Tile choice by shape (measured on MI355X with the encoder's products):
 // 256x256x64 tiles, two LDS stages, 8 waves of 128x64, fragment reads
 // pipelined across K tiles, wherever K is a multiple of 64 and at least 512
-// tiles exist; otherwise 256x128x32 with three stages (8 waves of 64x64), and
-// 128x128x32 with four stages when even those tiles would be too few to fill
-// the chip.  K not a multiple of 32 (the 80-mel first convolution) takes the
-// register-path kernel, which zero-fills the K tail.
+// tiles exist -- persistent (epilogue overlapped with the next tile's loads)
+// unless the epilogue reads the output (residual add); otherwise 256x128x32
+// with three stages (8 waves of 64x64), and 128x128x32 with four stages when
+// even those tiles would be too few to fill the chip.  K not a multiple of 32
+// (the 80-mel first convolution) takes the register-path kernel, which
+// zero-fills the K tail.
 template <int KIND>
 static void launch_gemm_bf16(const AView& a, const bf16_t* w, int M, int N, int K,
                              const Epilogue& e, hipStream_t s) {
@@ -731,7 +1061,14 @@ static void launch_gemm_bf16(const AView& a, const bf16_t* w, int M, int N, int 
     else
       launch_gemm_cfg<128, 128, 32, 2, 2, KIND>(a, w, M, N, K, e, s, 8);
   } else if (K % 64 == 0 && t256x256 >= 512) {
-    launch_gemm_pf<256, 256, 64, 2, 4, 2, KIND>(a, w, M, N, K, e, s, 4);
+    // (the scatter epilogues of the stem and of the fused QKV product run
+    // slower from the persistent kernel's half-block stage than from the
+    // plain kernel's full-block one)
+    if (KIND != EPI_RESID && KIND != EPI_QKV && KIND != EPI_CONV1 &&
+        fits_u32_offsets(a, M, N, K))
+      launch_gemm_ps<256, 256, 64, 2, 4, 2, KIND>(a, w, M, N, K, e, s, 4);
+    else
+      launch_gemm_pf<256, 256, 64, 2, 4, 2, KIND>(a, w, M, N, K, e, s, 4);
   } else if (t256x128 >= 512) {
     launch_gemm_pf<256, 128, 32, 4, 2, 3, KIND>(a, w, M, N, K, e, s, 4);
   } else {
@@ -750,6 +1087,7 @@ void gemm_bf16(const AView& a, const bf16_t* w, int M, int N, int K, const Epilo
     case EPI_CONV2: launch_gemm_bf16<EPI_CONV2>(a, w, M, N, K, e, s); break;
     case EPI_XKV: launch_gemm_bf16<EPI_XKV>(a, w, M, N, K, e, s); break;
     case EPI_QKV: launch_gemm_bf16<EPI_QKV>(a, w, M, N, K, e, s); break;
+    case EPI_F32: launch_gemm_bf16<EPI_F32>(a, w, M, N, K, e, s); break;
   }
 }
 
@@ -818,6 +1156,7 @@ void gemm_f32(const AView& a, const float* w, int M, int N, int K, const Epilogu
     case EPI_CONV1: launch_gemm_f32<EPI_CONV1>(a, w, M, N, K, e, s); break;
     case EPI_CONV2: launch_gemm_f32<EPI_CONV2>(a, w, M, N, K, e, s); break;
     case EPI_XKV: launch_gemm_f32<EPI_XKV>(a, w, M, N, K, e, s); break;
+    case EPI_F32: launch_gemm_f32<EPI_F32>(a, w, M, N, K, e, s); break;
   }
 }
 

@@ -99,50 +99,77 @@ template void copy_rows_from_f32<bf16_t>(const float*, int64_t, bf16_t*, int64_t
                                          hipStream_t);
 
 // ---------------------------------------------------------------------------
-// LayerNorm: one wave per row, biased variance, eps 1e-5.
+// LayerNorm: one wave per row, biased variance, eps 1e-5.  With RES the
+// residual branch y is first added into the stream (x += y, written back).
+// Rows of d = 256 * Q floats move as float4 (Q per lane).
 // ---------------------------------------------------------------------------
-template <typename T, int VPL>
-__global__ __launch_bounds__(256) void k_layer_norm(const float* x, int rows, const float* g,
-                                                    const float* b, T* out) {
-  constexpr int d = VPL * 64;
+template <typename T>
+__device__ __forceinline__ void st4(T* p, float4 v);
+template <>
+__device__ __forceinline__ void st4<float>(float* p, float4 v) {
+  *(float4*)p = v;
+}
+template <>
+__device__ __forceinline__ void st4<bf16_t>(bf16_t* p, float4 v) {
+  uint2 u;
+  u.x = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
+  u.y = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
+  *(uint2*)p = u;
+}
+
+template <typename T, int Q, bool RES>
+__global__ __launch_bounds__(256) void k_layer_norm(float* x, const float* y, int rows,
+                                                    const float* g, const float* b, T* out) {
+  constexpr int d = Q * 256;
   int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   int lane = threadIdx.x & 63;
   if (row >= rows) return;
-  const float* xr = x + (int64_t)row * d;
-  float v[VPL];
+  float* xr = x + (int64_t)row * d;
+  float4 v[Q];
   float s = 0.f;
 #pragma unroll
-  for (int i = 0; i < VPL; ++i) {
-    v[i] = xr[lane + 64 * i];
-    s += v[i];
+  for (int i = 0; i < Q; ++i) {
+    const int e = (lane + 64 * i) * 4;
+    v[i] = *(const float4*)(xr + e);
+    if constexpr (RES) {
+      const float4 t = *(const float4*)(y + (int64_t)row * d + e);
+      v[i] = make_float4(v[i].x + t.x, v[i].y + t.y, v[i].z + t.z, v[i].w + t.w);
+      *(float4*)(xr + e) = v[i];
+    }
+    s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
   }
   float mean = wave_sum(s) * (1.0f / d);
   float q = 0.f;
 #pragma unroll
-  for (int i = 0; i < VPL; ++i) {
-    v[i] -= mean;
-    q += v[i] * v[i];
+  for (int i = 0; i < Q; ++i) {
+    v[i] = make_float4(v[i].x - mean, v[i].y - mean, v[i].z - mean, v[i].w - mean);
+    q += (v[i].x * v[i].x + v[i].y * v[i].y) + (v[i].z * v[i].z + v[i].w * v[i].w);
   }
   float rstd = rsqrtf(wave_sum(q) * (1.0f / d) + 1e-5f);
   T* o = out + (int64_t)row * d;
 #pragma unroll
-  for (int i = 0; i < VPL; ++i) {
-    int e = lane + 64 * i;
-    St<T>::st(o, e, v[i] * rstd * g[e] + b[e]);
+  for (int i = 0; i < Q; ++i) {
+    const int e = (lane + 64 * i) * 4;
+    const float4 gg = *(const float4*)(g + e), bb = *(const float4*)(b + e);
+    st4<T>(o + e, make_float4(v[i].x * rstd * gg.x + bb.x, v[i].y * rstd * gg.y + bb.y,
+                              v[i].z * rstd * gg.z + bb.z, v[i].w * rstd * gg.w + bb.w));
   }
 }
 
 // Any d that is a multiple of 64: two passes over global memory.
-template <typename T>
-__global__ __launch_bounds__(256) void k_layer_norm_any(const float* x, int rows, int d,
-                                                        const float* g, const float* b,
+template <typename T, bool RES>
+__global__ __launch_bounds__(256) void k_layer_norm_any(float* x, const float* y, int rows,
+                                                        int d, const float* g, const float* b,
                                                         T* out) {
   int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   int lane = threadIdx.x & 63;
   if (row >= rows) return;
-  const float* xr = x + (int64_t)row * d;
+  float* xr = x + (int64_t)row * d;
   float s = 0.f;
-  for (int e = lane; e < d; e += 64) s += xr[e];
+  for (int e = lane; e < d; e += 64) {
+    if constexpr (RES) xr[e] += y[(int64_t)row * d + e];
+    s += xr[e];
+  }
   float mean = wave_sum(s) / d;
   float q = 0.f;
   for (int e = lane; e < d; e += 64) {
@@ -154,20 +181,35 @@ __global__ __launch_bounds__(256) void k_layer_norm_any(const float* x, int rows
   for (int e = lane; e < d; e += 64) St<T>::st(o, e, (xr[e] - mean) * rstd * g[e] + b[e]);
 }
 
-template <typename T>
-void layer_norm(const float* x, int rows, int d, const float* g, const float* b, T* out,
-                hipStream_t s) {
+template <typename T, bool RES>
+static void layer_norm_launch(float* x, const float* y, int rows, int d, const float* g,
+                              const float* b, T* out, hipStream_t s) {
   if (rows <= 0) return;
   dim3 grid((rows + 3) / 4);
   switch (d) {
-    case 384: k_layer_norm<T, 6><<<grid, 256, 0, s>>>(x, rows, g, b, out); break;
-    case 512: k_layer_norm<T, 8><<<grid, 256, 0, s>>>(x, rows, g, b, out); break;
-    case 768: k_layer_norm<T, 12><<<grid, 256, 0, s>>>(x, rows, g, b, out); break;
-    case 1024: k_layer_norm<T, 16><<<grid, 256, 0, s>>>(x, rows, g, b, out); break;
-    case 1280: k_layer_norm<T, 20><<<grid, 256, 0, s>>>(x, rows, g, b, out); break;
-    default: k_layer_norm_any<T><<<grid, 256, 0, s>>>(x, rows, d, g, b, out); break;
+    case 512: k_layer_norm<T, 2, RES><<<grid, 256, 0, s>>>(x, y, rows, g, b, out); break;
+    case 768: k_layer_norm<T, 3, RES><<<grid, 256, 0, s>>>(x, y, rows, g, b, out); break;
+    case 1024: k_layer_norm<T, 4, RES><<<grid, 256, 0, s>>>(x, y, rows, g, b, out); break;
+    case 1280: k_layer_norm<T, 5, RES><<<grid, 256, 0, s>>>(x, y, rows, g, b, out); break;
+    default: k_layer_norm_any<T, RES><<<grid, 256, 0, s>>>(x, y, rows, d, g, b, out); break;
   }
 }
+
+template <typename T>
+void layer_norm(const float* x, int rows, int d, const float* g, const float* b, T* out,
+                hipStream_t s) {
+  layer_norm_launch<T, false>(const_cast<float*>(x), nullptr, rows, d, g, b, out, s);
+}
+
+template <typename T>
+void residual_layer_norm(float* x, const float* y, int rows, int d, const float* g,
+                         const float* b, T* out, hipStream_t s) {
+  layer_norm_launch<T, true>(x, y, rows, d, g, b, out, s);
+}
+template void residual_layer_norm<float>(float*, const float*, int, int, const float*,
+                                         const float*, float*, hipStream_t);
+template void residual_layer_norm<bf16_t>(float*, const float*, int, int, const float*,
+                                          const float*, bf16_t*, hipStream_t);
 template void layer_norm<float>(const float*, int, int, const float*, const float*, float*,
                                 hipStream_t);
 template void layer_norm<bf16_t>(const float*, int, int, const float*, const float*, bf16_t*,

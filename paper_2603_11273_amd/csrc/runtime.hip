@@ -493,10 +493,10 @@ template <typename T>
 void gemm_any(asr_ctx* c, const AView& a, size_t w_off, int M, int N, int K, const Epilogue& e) {
   double flops = 2.0 * M * N * K;
   // operands read once, result written once; the fp32 residual epilogue also
-  // reads the residual, the second convolution writes fp32
+  // reads the residual, the second convolution and EPI_F32 write fp32
   double out_bytes = (double)M * N * c->es;
   if (e.kind == EPI_RESID) out_bytes = 2.0 * M * N * 4;
-  if (e.kind == EPI_CONV2) out_bytes = (double)M * N * 4;
+  if (e.kind == EPI_CONV2 || e.kind == EPI_F32) out_bytes = (double)M * N * 4;
   double bytes = (double)M * K * c->es + (double)N * K * c->es + out_bytes;
   timed(c, ASR_K_GEMM, flops, bytes, [&] {
     if (c->bf16())
@@ -511,6 +511,16 @@ void ln_any(asr_ctx* c, const float* x, int rows, size_t g, size_t b, T* out) {
   const int d = c->cfg.d_model;
   timed(c, ASR_K_LN, 8.0 * rows * d, (double)rows * d * (4 + c->es), [&] {
     layer_norm<T>(x, rows, d, c->at<float>(g), c->at<float>(b), out, c->stream);
+  });
+}
+
+// x += y, then out = LayerNorm(x): the residual add of a block fused with the
+// LayerNorm that follows it.
+template <typename T>
+void res_ln_any(asr_ctx* c, float* x, const float* y, int rows, size_t g, size_t b, T* out) {
+  const int d = c->cfg.d_model;
+  timed(c, ASR_K_LN, 9.0 * rows * d, (double)rows * d * (12 + c->es), [&] {
+    residual_layer_norm<T>(x, y, rows, d, c->at<float>(g), c->at<float>(b), out, c->stream);
   });
 }
 
@@ -553,9 +563,15 @@ asr_status encode_clips(asr_ctx* c, int n) {
   T* qkv = c->at<T>(L.qkv);
   T* att = c->at<T>(L.att);
   T* hid = c->at<T>(L.hid);
+  // The residual branches (attention out-projection, FC2) are written in
+  // float32 to y, which borrows the QKV buffer (dead once attention has run,
+  // and at least 4 d bytes per row in either dtype); the LayerNorm kernel that
+  // follows adds y into the stream.
+  float* y = c->at<float>(L.qkv);
+  if (g.n_enc > 0) ln_any<T>(c, x, R, L.enc[0].ln1_g, L.enc[0].ln1_b, xn);
   for (int l = 0; l < g.n_enc; ++l) {
     const EncLayer& w = L.enc[l];
-    ln_any<T>(c, x, R, w.ln1_g, w.ln1_b, xn);
+    // xn holds LN_1(x) here
     {
       // bf16: q, k into the fused buffer and v transposed per head for the
       // flash-attention kernel; fp32: plain [R][3d]
@@ -581,13 +597,13 @@ asr_status encode_clips(asr_ctx* c, int n) {
     {
       AView a{att, d, 0, R};
       Epilogue e{};
-      e.kind = EPI_RESID;
-      e.out = x;
+      e.kind = EPI_F32;
+      e.out = y;
       e.ldc = d;
       e.bias = c->at<float>(w.o_b);
       gemm_any<T>(c, a, w.o_w, R, d, d, e);
     }
-    ln_any<T>(c, x, R, w.ln2_g, w.ln2_b, xn);
+    res_ln_any<T>(c, x, y, R, w.ln2_g, w.ln2_b, xn);
     {
       AView a{xn, d, 0, R};
       Epilogue e{};
@@ -600,14 +616,18 @@ asr_status encode_clips(asr_ctx* c, int n) {
     {
       AView a{hid, F, 0, R};
       Epilogue e{};
-      e.kind = EPI_RESID;
-      e.out = x;
+      e.kind = EPI_F32;
+      e.out = y;
       e.ldc = d;
       e.bias = c->at<float>(w.fc2_b);
       gemm_any<T>(c, a, w.fc2_w, R, d, F, e);
     }
+    // the next LayerNorm: the next layer's LN_1, or ln_post after the last layer
+    const bool last = l + 1 == g.n_enc;
+    res_ln_any<T>(c, x, y, R, last ? L.lnp_g : L.enc[l + 1].ln1_g,
+                  last ? L.lnp_b : L.enc[l + 1].ln1_b, xn);
   }
-  ln_any<T>(c, x, R, L.lnp_g, L.lnp_b, xn);
+  if (g.n_enc == 0) ln_any<T>(c, x, R, L.lnp_g, L.lnp_b, xn);
   CHECK_LAUNCH();
   return ASR_OK;
 }
