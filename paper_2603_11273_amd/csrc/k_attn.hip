@@ -22,9 +22,6 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) {
   __builtin_memcpy(&r, &u, 16);
   return r;
 }
-__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
-}
 
 // ---------------------------------------------------------------------------
 // Encoder flash attention (bf16)
@@ -146,10 +143,23 @@ __global__ __launch_bounds__(NW * 64) void k_flash_bf16(const bf16_t* __restrict
 #pragma unroll
       for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, s[kb][r]);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float mnew = fmaxf(m, tmax);
-    const float alpha = exp2f((m - mnew) * sc);
-    const float nb = -mnew * sc;
-    m = mnew;
+    // Lazy rescaling: the running reference m only moves (and O, l are only
+    // rescaled) when some query of the wave sees a score more than 2^8 above
+    // it in the exp2 domain.  Until then the probabilities exp2((s - m) sc)
+    // may exceed 1 by up to 256x, which fp32 sums and bf16 operands carry
+    // with unchanged relative precision; the final 1/l cancels the offset.
+    if (__any((tmax - m) * sc > 8.0f)) {
+      const float mnew = fmaxf(m, tmax);
+      const float alpha = __builtin_amdgcn_exp2f((m - mnew) * sc);   // 0 on the first tile
+      m = mnew;
+      l *= alpha;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        o0[r] *= alpha;
+        o1[r] *= alpha;
+      }
+    }
+    const float nb = -m * sc;
     float psum = 0.f;
     bf16x8 pb[2][2];                               // [kb][hf]
 #pragma unroll
@@ -159,19 +169,16 @@ __global__ __launch_bounds__(NW * 64) void k_flash_bf16(const bf16_t* __restrict
         float p[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          p[i] = exp2f(fmaf(s[kb][hf * 8 + i], sc, nb));
+          // exp2 of a value <= 8; results below 2^-126 flush to 0, far below
+          // the bf16 resolution of a probability next to the row's maximum
+          p[i] = __builtin_amdgcn_exp2f(fmaf(s[kb][hf * 8 + i], sc, nb));
           psum += p[i];
         }
-        uint4 u = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
-                   pack_bf16x2(p[6], p[7])};
+        uint4 u = {pack2_bf16(p[0], p[1]), pack2_bf16(p[2], p[3]), pack2_bf16(p[4], p[5]),
+                   pack2_bf16(p[6], p[7])};
         pb[kb][hf] = as_bf16x8(u);
       }
-    l = l * alpha + psum;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      o0[r] *= alpha;
-      o1[r] *= alpha;
-    }
+    l += psum;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -201,10 +208,10 @@ __global__ __launch_bounds__(NW * 64) void k_flash_bf16(const bf16_t* __restrict
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
     const int d0 = g * 8 + half * 4;
-    uint2 w0 = {pack_bf16x2(o0[g * 4 + 0] * inv, o0[g * 4 + 1] * inv),
-                pack_bf16x2(o0[g * 4 + 2] * inv, o0[g * 4 + 3] * inv)};
-    uint2 w1 = {pack_bf16x2(o1[g * 4 + 0] * inv, o1[g * 4 + 1] * inv),
-                pack_bf16x2(o1[g * 4 + 2] * inv, o1[g * 4 + 3] * inv)};
+    uint2 w0 = {pack2_bf16(o0[g * 4 + 0] * inv, o0[g * 4 + 1] * inv),
+                pack2_bf16(o0[g * 4 + 2] * inv, o0[g * 4 + 3] * inv)};
+    uint2 w1 = {pack2_bf16(o1[g * 4 + 0] * inv, o1[g * 4 + 1] * inv),
+                pack2_bf16(o1[g * 4 + 2] * inv, o1[g * 4 + 3] * inv)};
     *(uint2*)(op + d0) = w0;
     *(uint2*)(op + 32 + d0) = w1;
   }

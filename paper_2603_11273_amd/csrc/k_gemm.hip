@@ -72,8 +72,8 @@ __device__ __forceinline__ void epi_apply(const Epilogue& e, int r, int n, float
 __device__ __forceinline__ void st4_bf16(bf16_t* p, float4 v) {
   typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
   u32x2 u;
-  u.x = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
-  u.y = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
+  u.x = pack2_bf16(v.x, v.y);
+  u.y = pack2_bf16(v.z, v.w);
   __builtin_nontemporal_store(u, (u32x2*)p);
 }
 __device__ __forceinline__ void st4_f32(float* p, float4 v) {

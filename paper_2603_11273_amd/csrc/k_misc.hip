@@ -112,8 +112,8 @@ __device__ __forceinline__ void st4<float>(float* p, float4 v) {
 template <>
 __device__ __forceinline__ void st4<bf16_t>(bf16_t* p, float4 v) {
   uint2 u;
-  u.x = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
-  u.y = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
+  u.x = pack2_bf16(v.x, v.y);
+  u.y = pack2_bf16(v.z, v.w);
   *(uint2*)p = u;
 }
 
