@@ -1066,7 +1066,7 @@ static void launch_gemm_bf16(const AView& a, const bf16_t* w, int M, int N, int 
     // plain kernel's full-block one)
     if (KIND != EPI_RESID && KIND != EPI_QKV && KIND != EPI_CONV1 &&
         fits_u32_offsets(a, M, N, K))
-      launch_gemm_ps<256, 256, 64, 2, 4, 2, KIND>(a, w, M, N, K, e, s, 4);
+      launch_gemm_ps<256, 256, 64, 2, 4, 2, KIND>(a, w, M, N, K, e, s, N >= 3072 ? 8 : 4);
     else
       launch_gemm_pf<256, 256, 64, 2, 4, 2, KIND>(a, w, M, N, K, e, s, 4);
   } else if (t256x128 >= 512) {
