@@ -199,6 +199,84 @@ typedef enum {
   ASR_K_COUNT = 10
 } asr_kernel_class;
 
+/* ---------------------------------------------------------------------------
+ * Continuous batching with preemption (the serving loop the scheduling policy
+ * runs in: Section 4.1's engine setup, and the preemption rule of the
+ * implementation appendix).
+ *
+ * Each engine step at now_us: (1) every running request is about to decode
+ * one token; while the KV pool cannot hold that, a running request is
+ * preempted -- SJF the one with the largest job key, HRRN the one with the
+ * lowest current response ratio (wait + job) / job, FCFS the most recently
+ * admitted -- and goes back to the waiting queue with its arrival time and
+ * keys (its tokens are dropped: it is recomputed when admitted again);
+ * (2) free slots are refilled from the queue in the policy's order, each
+ * admitted request being prefilled and producing its first token in this
+ * step, until max_admit, no free slot, or the first request the pool cannot
+ * hold; (3) all running requests decode one token (greedy: the argmax becomes
+ * the next input) and those that reach their token count finish.
+ *
+ * A request produces round-half-up(duration * tok_num / tok_den) tokens,
+ * clamped to [1, min(448, max_tokens)].  The pool counts token positions: a
+ * running request holds cross_tokens plus one per generated token.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+  int64_t kv_capacity;  /* pool size in token positions; <= 0: slots are the only bound;
+                           otherwise >= cross_tokens + 448 */
+  int32_t cross_tokens; /* positions charged for a request's cross cache (1500) */
+  int32_t max_admit;    /* admissions per step, 1 .. max_prefill */
+  int32_t tok_num;      /* output tokens per audio-second = tok_num / tok_den (27/10) */
+  int32_t tok_den;
+  int32_t start_token;  /* decoder input at position 0 */
+} asr_serve_cfg;
+
+/* Arrays are the caller's, each with room for cap >= the slot count
+ * (min(max_slots, max_decode) on a GPU context, max_slots queue-only). */
+typedef struct {
+  int32_t cap;
+  int64_t* preempted;     int32_t n_preempted;
+  int64_t* admitted;      int32_t* admitted_slot;  int32_t n_admitted;
+  int64_t* decoded;       int32_t* token;          int32_t n_decoded;  /* token -1: no model ran */
+  int64_t* finished;      int32_t n_finished;
+} asr_serve_out;
+
+/* Switches the context to continuous batching (the manual asr_pop_batch /
+ * asr_step / asr_release_slot then return ESTATE).  ESTATE when slots are
+ * occupied or popped requests wait; EINVAL for an inconsistent config. */
+asr_status asr_serve_config(asr_ctx* ctx, const asr_serve_cfg* cfg);
+/* One engine step on the GPU: plan, prefill the admitted requests, decode
+ * every running request, commit.  Synchronises on the bound stream. */
+asr_status asr_serve_step(asr_ctx* ctx, int64_t now_us, asr_serve_out* out);
+/* The same schedule without running the model (tokens -1), for queue-only
+ * contexts (device = -1; ESTATE otherwise): simulations and CPU tests. */
+asr_status asr_serve_plan(asr_ctx* ctx, int64_t now_us, asr_serve_out* out);
+/* Tokens of a finished request, once (ENOTFOUND otherwise; EINVAL when cap is
+ * smaller than the token count). */
+asr_status asr_serve_tokens(asr_ctx* ctx, int64_t id, int32_t* tokens, int32_t cap, int32_t* n);
+
+/* Serving simulation (the evaluation of Section 4.1 and the burst appendix on
+ * a virtual clock).  A step that admits a requests and decodes r rows lasts
+ * prefill_us * a + (r > 0 ? step_us + row_us * r : 0) microseconds. */
+typedef struct {
+  int64_t prefill_us;
+  int64_t step_us;
+  int64_t row_us;
+} asr_sim_cost;
+/* Runs the continuous-batching schedule (asr_serve_plan steps) from t0_us,
+ * jumping over idle time to the next arrival, until every submitted request
+ * has finished.  Queue-only, serve-configured contexts; ids lists every
+ * submitted request (EINVAL otherwise).  Per request ids[i]: time of its first
+ * and last token (first_us, finish_us), token count and preemptions; token_us
+ * (may be NULL) receives the emission time of every token, request after
+ * request in ids order (token_cap entries at least; a position that a
+ * recomputed request produces again is not emitted again).  *t_end_us is the
+ * clock after the last step.  Latencies follow: TTFT = first_us - arrival,
+ * E2EL = finish_us - arrival. */
+asr_status asr_serve_simulate(asr_ctx* ctx, const asr_sim_cost* cost, int64_t t0_us, int32_t n,
+                              const int64_t* ids, int64_t* first_us, int64_t* finish_us,
+                              int32_t* n_tokens, int32_t* n_preempt, int64_t* token_us,
+                              int64_t token_cap, int64_t* t_end_us);
+
 /* classes is a bit mask over the asr_kernel_class values: bit k selects class
  * k, 0 turns timing off, ASR_TIME_ALL times every class.  An event pair is
  * recorded on the context's stream around every launch (and phase) of a

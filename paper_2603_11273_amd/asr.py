@@ -29,7 +29,8 @@ EXPORTED = [
     "asr_rank", "asr_pop_batch", "asr_queue_len", "asr_step", "asr_release_slot",
     "asr_slot_info", "asr_set_timing", "asr_get_timing", "asr_reset_timing",
     "asr_debug_logmel", "asr_debug_encode", "asr_debug_set_encoder_out", "asr_debug_get_kv",
-    "asr_debug_set_self_kv",
+    "asr_debug_set_self_kv", "asr_serve_config", "asr_serve_step", "asr_serve_plan",
+    "asr_serve_tokens", "asr_serve_simulate",
 ]
 
 
@@ -48,6 +49,26 @@ class StepIn(C.Structure):
 class StepOut(C.Structure):
     _fields_ = [("slot_of", C.POINTER(C.c_int32)), ("argmax", C.POINTER(C.c_int32)),
                 ("done", C.POINTER(C.c_int32))]
+
+
+class ServeCfg(C.Structure):
+    _fields_ = [("kv_capacity", C.c_int64), ("cross_tokens", C.c_int32),
+                ("max_admit", C.c_int32), ("tok_num", C.c_int32), ("tok_den", C.c_int32),
+                ("start_token", C.c_int32)]
+
+
+class ServeOut(C.Structure):
+    _fields_ = [("cap", C.c_int32),
+                ("preempted", C.POINTER(C.c_int64)), ("n_preempted", C.c_int32),
+                ("admitted", C.POINTER(C.c_int64)), ("admitted_slot", C.POINTER(C.c_int32)),
+                ("n_admitted", C.c_int32),
+                ("decoded", C.POINTER(C.c_int64)), ("token", C.POINTER(C.c_int32)),
+                ("n_decoded", C.c_int32),
+                ("finished", C.POINTER(C.c_int64)), ("n_finished", C.c_int32)]
+
+
+class SimCost(C.Structure):
+    _fields_ = [("prefill_us", C.c_int64), ("step_us", C.c_int64), ("row_us", C.c_int64)]
 
 
 class AsrError(RuntimeError):
@@ -95,6 +116,12 @@ def _load():
         "asr_debug_set_encoder_out": [vp, P(i32), P(i64), P(i32), i32, vp, i32],
         "asr_debug_get_kv": [vp, i32, i32, P(f)],
         "asr_debug_set_self_kv": [vp, i32, vp, i32, i32],
+        "asr_serve_config": [vp, P(ServeCfg)],
+        "asr_serve_step": [vp, i64, P(ServeOut)],
+        "asr_serve_plan": [vp, i64, P(ServeOut)],
+        "asr_serve_tokens": [vp, i64, P(i32), i32, P(i32)],
+        "asr_serve_simulate": [vp, P(SimCost), i64, i32, P(i64), P(i64), P(i64), P(i32),
+                               P(i32), P(i64), i64, P(i64)],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -150,6 +177,7 @@ class Context:
         self.h = h
         self._block = None
         self._keep = []
+        self._serve_cap = max(cfg.max_slots, 1)
 
     def close(self):
         if self.h:
@@ -250,6 +278,74 @@ class Context:
 
     def release_slot(self, slot):
         _check(lib.asr_release_slot(self.h, slot))
+
+    # -- continuous batching ----------------------------------------------------
+    def serve_config(self, kv_capacity=0, cross_tokens=1500, max_admit=1, tok_num=27,
+                     tok_den=10, start_token=0):
+        cfg = ServeCfg(kv_capacity, cross_tokens, max_admit, tok_num, tok_den, start_token)
+        _check(lib.asr_serve_config(self.h, C.byref(cfg)))
+        self._serve_cap = max(self.cfg.max_slots, 1)
+
+    def _serve(self, fn, now_us):
+        cap = self._serve_cap
+        bufs = {k: np.zeros(cap, np.int64) for k in ("preempted", "admitted", "decoded", "finished")}
+        slot = np.zeros(cap, np.int32)
+        tok = np.zeros(cap, np.int32)
+        p64 = lambda a: a.ctypes.data_as(C.POINTER(C.c_int64))  # noqa: E731
+        p32 = lambda a: a.ctypes.data_as(C.POINTER(C.c_int32))  # noqa: E731
+        out = ServeOut(cap, p64(bufs["preempted"]), 0, p64(bufs["admitted"]), p32(slot), 0,
+                       p64(bufs["decoded"]), p32(tok), 0, p64(bufs["finished"]), 0)
+        _check(fn(self.h, now_us, C.byref(out)))
+        return {"preempted": bufs["preempted"][:out.n_preempted].tolist(),
+                "admitted": bufs["admitted"][:out.n_admitted].tolist(),
+                "admitted_slot": slot[:out.n_admitted].tolist(),
+                "decoded": bufs["decoded"][:out.n_decoded].tolist(),
+                "token": tok[:out.n_decoded].tolist(),
+                "finished": bufs["finished"][:out.n_finished].tolist()}
+
+    def serve_step(self, now_us):
+        """One continuous-batching step on the GPU (see asr_serve_step)."""
+        return self._serve(lib.asr_serve_step, now_us)
+
+    def serve_plan(self, now_us):
+        """The same schedule without the model (queue-only contexts)."""
+        return self._serve(lib.asr_serve_plan, now_us)
+
+    def serve_simulate(self, ids, prefill_us, step_us, row_us, t0_us=0, want_token_times=True,
+                       token_cap=None):
+        """Virtual-clock serving run (asr_serve_simulate).  Returns
+        ({id: {first_us, finish_us, n_tokens, n_preempt, token_us}}, t_end_us)."""
+        n = len(ids)
+        ids_a = np.asarray(ids, np.int64)
+        first = np.zeros(max(n, 1), np.int64)
+        fin = np.zeros(max(n, 1), np.int64)
+        ntok = np.zeros(max(n, 1), np.int32)
+        npre = np.zeros(max(n, 1), np.int32)
+        cap = token_cap if token_cap is not None else 448 * max(n, 1)
+        tok = np.zeros(cap, np.int64) if want_token_times else None
+        t_end = C.c_int64()
+        p64 = lambda a: a.ctypes.data_as(C.POINTER(C.c_int64))  # noqa: E731
+        p32 = lambda a: a.ctypes.data_as(C.POINTER(C.c_int32))  # noqa: E731
+        cost = SimCost(prefill_us, step_us, row_us)
+        _check(lib.asr_serve_simulate(self.h, C.byref(cost), t0_us, n, p64(ids_a), p64(first),
+                                      p64(fin), p32(ntok), p32(npre),
+                                      p64(tok) if tok is not None else None, cap,
+                                      C.byref(t_end)))
+        out, off = {}, 0
+        for i, rid in enumerate(ids):
+            k = int(ntok[i])
+            out[int(rid)] = {"first_us": int(first[i]), "finish_us": int(fin[i]), "n_tokens": k,
+                             "n_preempt": int(npre[i]),
+                             "token_us": tok[off:off + k].tolist() if tok is not None else None}
+            off += k
+        return out, t_end.value
+
+    def serve_tokens(self, rid):
+        buf = np.zeros(448, np.int32)
+        n = C.c_int32()
+        _check(lib.asr_serve_tokens(self.h, rid, buf.ctypes.data_as(C.POINTER(C.c_int32)), 448,
+                                    C.byref(n)))
+        return buf[:n.value].tolist()
 
     def slot_info(self, slot):
         occ, rid, pos, left = C.c_int32(), C.c_int64(), C.c_int32(), C.c_int32()

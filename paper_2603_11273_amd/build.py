@@ -19,7 +19,7 @@ LIB = os.path.join(HERE, "libasr_mi355x.so")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 
 HIP_SOURCES = ["k_misc.hip", "k_gemm.hip", "k_attn.hip", "runtime.hip"]
-CPP_SOURCES = ["queue.cpp"]
+CPP_SOURCES = ["queue.cpp", "serve.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # packed fp32 instructions are disabled: hipcc emits them from plain float
 # code at -O3 and we keep all fp32 arithmetic scalar.

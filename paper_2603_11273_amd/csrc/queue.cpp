@@ -99,4 +99,16 @@ std::vector<QEntry> WaitQueue::pop_batch(int64_t now_us, int max_n) {
   return out;
 }
 
+bool WaitQueue::any_eligible(int64_t now_us) const {
+  for (const auto& e : items_)
+    if (e.arrival_us <= now_us) return true;
+  return false;
+}
+
+int64_t WaitQueue::min_arrival() const {
+  int64_t m = INT64_MAX;
+  for (const auto& e : items_) m = std::min(m, e.arrival_us);
+  return m;
+}
+
 }  // namespace asr

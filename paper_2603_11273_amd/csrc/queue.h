@@ -45,6 +45,8 @@ class WaitQueue {
   void push(QEntry e);
   std::vector<int64_t> rank(int64_t now_us) const;
   std::vector<QEntry> pop_batch(int64_t now_us, int max_n);
+  bool any_eligible(int64_t now_us) const;
+  int64_t min_arrival() const;   // INT64_MAX when empty
 
  private:
   int64_t job_of(const QEntry& e) const;

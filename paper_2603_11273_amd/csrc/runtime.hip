@@ -12,6 +12,7 @@
 #include "../../include/asr.h"
 #include "asr_kernels.h"
 #include "queue.h"
+#include "serve.h"
 
 using namespace asr;
 
@@ -108,6 +109,11 @@ struct asr_ctx {
   std::unordered_map<int64_t, Request> waiting;   // submitted, not popped
   std::unordered_map<int64_t, Request> popped;    // popped, not prefilled
   std::vector<Slot> slots;
+  // continuous batching (asr_serve_*): the engine owns the slots while on
+  ServeEngine serve;
+  bool serve_mode = false;
+  std::unordered_map<int64_t, Request> serving;   // admitted, not finished (audio kept
+                                                  // for a re-prefill after preemption)
   Layout L;
   bool bound = false, loaded = false;
   char* base = nullptr;
@@ -929,7 +935,8 @@ asr_status asr_submit(asr_ctx* c, int64_t id, const float* pcm, int64_t n_sample
   if (n_samples == 0 && (pcm != nullptr || duration_us <= 0))
     return fail(ASR_EINVAL, "a request without samples needs pcm = NULL and duration_us > 0");
   if (max_tokens > kTextCtx) return fail(ASR_EINVAL, "max_tokens must be <= 448");
-  if (c->queue.contains(id) || c->waiting.count(id) || c->popped.count(id))
+  if (c->queue.contains(id) || c->waiting.count(id) || c->popped.count(id) ||
+      c->serving.count(id) || c->serve.has_result(id))
     return fail(ASR_EINVAL, "duplicate request id " + std::to_string(id));
   if ((int64_t)c->queue.size() >= c->cfg.max_queue) return fail(ASR_EFULL, "queue full");
   Request r;
@@ -963,6 +970,7 @@ asr_status asr_rank(const asr_ctx* c, int64_t now_us, int64_t* out_ids, int32_t 
 
 asr_status asr_pop_batch(asr_ctx* c, int64_t now_us, int32_t max_n, int64_t* out_ids, int32_t* n_out) {
   if (!c || !n_out || (max_n > 0 && !out_ids)) return fail(ASR_EINVAL, "NULL argument");
+  if (c->serve_mode) return fail(ASR_ESTATE, "context is in continuous-batching mode (asr_serve_*)");
   std::vector<QEntry> got = c->queue.pop_batch(now_us, max_n);
   for (size_t i = 0; i < got.size(); ++i) {
     out_ids[i] = got[i].id;
@@ -982,6 +990,7 @@ asr_status asr_queue_len(const asr_ctx* c, int32_t* n) {
 
 asr_status asr_release_slot(asr_ctx* c, int32_t slot) {
   if (!c) return fail(ASR_EINVAL, "NULL context");
+  if (c->serve_mode) return fail(ASR_ESTATE, "context is in continuous-batching mode (asr_serve_*)");
   if (slot < 0 || slot >= c->cfg.max_slots) return fail(ASR_ENOTFOUND, "no such slot");
   c->slots[slot] = Slot();
   return ASR_OK;
@@ -999,10 +1008,86 @@ asr_status asr_slot_info(const asr_ctx* c, int32_t slot, int32_t* occupied, int6
   return ASR_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Step execution shared by asr_step and asr_serve_step
+// ---------------------------------------------------------------------------
+}  // extern "C"
+
+namespace {
+
+// Prefill: audio of reqs[i] -> mel -> stem -> encoder -> cross K/V of slot slots[i].
+asr_status run_prefill(asr_ctx* c, const std::vector<const Request*>& reqs,
+                       const std::vector<int32_t>& slots) {
+  const int P = (int)reqs.size();
+  if (P == 0) return ASR_OK;
+  hipStream_t s = c->stream;
+  std::vector<const float*> ptrs(P);
+  std::vector<int64_t> ns(P);
+  bool any_host = false;
+  for (int i = 0; i < P; ++i) {
+    ns[i] = reqs[i]->n_samples;
+    if (reqs[i]->dev_pcm) {
+      ptrs[i] = reqs[i]->dev_pcm;
+    } else {
+      // host clips are uploaded into staging; every clip then reads device memory
+      float* dst = c->at<float>(c->L.pcm_stage) + (size_t)i * kSamples30s;
+      HIPCHK(hipMemcpyAsync(dst, reqs[i]->pcm.data(), ns[i] * 4, hipMemcpyHostToDevice, s));
+      ptrs[i] = dst;
+      any_host = true;
+    }
+  }
+  HIPCHK(hipMemcpyAsync(c->at(c->L.pcm_ptrs), ptrs.data(), P * 8, hipMemcpyHostToDevice, s));
+  HIPCHK(hipMemcpyAsync(c->at(c->L.pcm_n), ns.data(), P * 8, hipMemcpyHostToDevice, s));
+  HIPCHK(hipMemcpyAsync(c->at(c->L.p_slots), slots.data(), P * 4, hipMemcpyHostToDevice, s));
+  PhaseMark pm(c, ASR_K_PREFILL);
+  asr_status st = c->bf16() ? encode_clips<bf16_t>(c, P) : encode_clips<float>(c, P);
+  if (st != ASR_OK) return st;
+  if (c->cfg.n_dec > 0) {
+    st = c->bf16() ? cross_kv<bf16_t>(c, c->at(c->L.xn), P) : cross_kv<float>(c, c->at(c->L.xn), P);
+    if (st != ASR_OK) return st;
+  }
+  pm.end();
+  // the pageable host vectors and the small pointer arrays above must outlive
+  // the copies that read them
+  HIPCHK(hipStreamSynchronize(s));
+  (void)any_host;
+  return ASR_OK;
+}
+
+// Decode rows (slot, token, position) -> argmax (and logits when asked).
+// Returns EDEVICE after the copies when a NaN logit was flagged.
+asr_status run_decode(asr_ctx* c, int D, const int32_t* slots, const int32_t* tokens,
+                      const std::vector<int32_t>& pos, int32_t* argmax, float* logits) {
+  if (D == 0) return ASR_OK;
+  hipStream_t s = c->stream;
+  HIPCHK(hipMemcpyAsync(c->at(c->L.d_slots), slots, D * 4, hipMemcpyHostToDevice, s));
+  HIPCHK(hipMemcpyAsync(c->at(c->L.d_tokens), tokens, D * 4, hipMemcpyHostToDevice, s));
+  HIPCHK(hipMemcpyAsync(c->at(c->L.d_pos), pos.data(), D * 4, hipMemcpyHostToDevice, s));
+  PhaseMark pm(c, ASR_K_DECODE);
+  asr_status st = c->bf16() ? decode_rows<bf16_t>(c, D, pos, logits != nullptr)
+                            : decode_rows<float>(c, D, pos, logits != nullptr);
+  if (st != ASR_OK) return st;
+  pm.end();
+  int32_t flag = 0;
+  HIPCHK(hipMemcpyAsync(argmax, c->at(c->L.d_argmax), D * 4, hipMemcpyDeviceToHost, s));
+  HIPCHK(hipMemcpyAsync(&flag, c->at(c->L.d_flag), 4, hipMemcpyDeviceToHost, s));
+  if (logits)
+    HIPCHK(hipMemcpyAsync(logits, c->at(c->L.d_logits), (size_t)D * c->cfg.vocab * 4,
+                          hipMemcpyDeviceToHost, s));
+  HIPCHK(hipStreamSynchronize(s));
+  if (flag) return fail(ASR_EDEVICE, "NaN logit");
+  return ASR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 asr_status asr_step(asr_ctx* c, const asr_step_in* in, asr_step_out* out) {
   asr_status st = need_gpu(c, true);
   if (st != ASR_OK) return st;
   if (!in || !out) return fail(ASR_EINVAL, "NULL argument");
+  if (c->serve_mode) return fail(ASR_ESTATE, "context is in continuous-batching mode (asr_serve_*)");
   const asr_model_cfg& g = c->cfg;
   const int P = in->n_prefill, D = in->n_decode;
   if (P < 0 || P > g.max_prefill) return fail(ASR_EINVAL, "n_prefill out of [0, max_prefill]");
@@ -1014,7 +1099,7 @@ asr_status asr_step(asr_ctx* c, const asr_step_in* in, asr_step_out* out) {
   if (D > 0 && g.n_dec == 0) return fail(ASR_EINVAL, "encoder-only context cannot decode");
   // validate prefill
   std::vector<int> taken;
-  std::vector<Request*> reqs;
+  std::vector<const Request*> reqs;
   for (int i = 0; i < P; ++i) {
     auto it = c->popped.find(in->prefill_ids[i]);
     if (it == c->popped.end())
@@ -1041,45 +1126,10 @@ asr_status asr_step(asr_ctx* c, const asr_step_in* in, asr_step_out* out) {
     if (pos[i] >= kTextCtx) return fail(ASR_EINVAL, "slot position reached 448");
   }
   HIPCHK(hipSetDevice(c->device));
-  hipStream_t s = c->stream;
   if (P > 0) {
-    std::vector<const float*> ptrs(P);
-    std::vector<int64_t> ns(P);
-    bool any_host = false, any_dev = false;
-    for (int i = 0; i < P; ++i) {
-      ns[i] = reqs[i]->n_samples;
-      if (reqs[i]->dev_pcm) {
-        ptrs[i] = reqs[i]->dev_pcm;
-        any_dev = true;
-      } else {
-        ptrs[i] = reqs[i]->pcm.data();
-        any_host = true;
-      }
-    }
-    // mixed host/device batches: upload the host clips into staging, then
-    // point every clip at device memory
-    if (any_host) {
-      for (int i = 0; i < P; ++i) {
-        if (reqs[i]->dev_pcm) continue;
-        float* dst = c->at<float>(c->L.pcm_stage) + (size_t)i * kSamples30s;
-        HIPCHK(hipMemcpyAsync(dst, ptrs[i], ns[i] * 4, hipMemcpyHostToDevice, s));
-        ptrs[i] = dst;
-      }
-    }
-    (void)any_dev;
-    HIPCHK(hipMemcpyAsync(c->at(c->L.pcm_ptrs), ptrs.data(), P * 8, hipMemcpyHostToDevice, s));
-    HIPCHK(hipMemcpyAsync(c->at(c->L.pcm_n), ns.data(), P * 8, hipMemcpyHostToDevice, s));
     std::vector<int32_t> sl(taken.begin(), taken.end());
-    HIPCHK(hipMemcpyAsync(c->at(c->L.p_slots), sl.data(), P * 4, hipMemcpyHostToDevice, s));
-    PhaseMark pm(c, ASR_K_PREFILL);
-    st = c->bf16() ? encode_clips<bf16_t>(c, P) : encode_clips<float>(c, P);
+    st = run_prefill(c, reqs, sl);
     if (st != ASR_OK) return st;
-    if (g.n_dec > 0) {
-      st = c->bf16() ? cross_kv<bf16_t>(c, c->at(c->L.xn), P) : cross_kv<float>(c, c->at(c->L.xn), P);
-      if (st != ASR_OK) return st;
-    }
-    pm.end();
-    if (any_host) HIPCHK(hipStreamSynchronize(s));   // host PCM buffers are freed below
     for (int i = 0; i < P; ++i) {
       Slot& sl2 = c->slots[taken[i]];
       sl2.occupied = 1;
@@ -1091,30 +1141,233 @@ asr_status asr_step(asr_ctx* c, const asr_step_in* in, asr_step_out* out) {
     }
   }
   if (D > 0) {
-    HIPCHK(hipMemcpyAsync(c->at(c->L.d_slots), in->slots, D * 4, hipMemcpyHostToDevice, s));
-    HIPCHK(hipMemcpyAsync(c->at(c->L.d_tokens), in->tokens, D * 4, hipMemcpyHostToDevice, s));
-    HIPCHK(hipMemcpyAsync(c->at(c->L.d_pos), pos.data(), D * 4, hipMemcpyHostToDevice, s));
-    bool want_logits = in->logits != nullptr;
-    PhaseMark pm(c, ASR_K_DECODE);
-    st = c->bf16() ? decode_rows<bf16_t>(c, D, pos, want_logits) : decode_rows<float>(c, D, pos, want_logits);
-    if (st != ASR_OK) return st;
-    pm.end();
-    int32_t flag = 0;
-    HIPCHK(hipMemcpyAsync(out->argmax, c->at(c->L.d_argmax), D * 4, hipMemcpyDeviceToHost, s));
-    HIPCHK(hipMemcpyAsync(&flag, c->at(c->L.d_flag), 4, hipMemcpyDeviceToHost, s));
-    if (want_logits)
-      HIPCHK(hipMemcpyAsync(in->logits, c->at(c->L.d_logits), (size_t)D * g.vocab * 4,
-                            hipMemcpyDeviceToHost, s));
-    HIPCHK(hipStreamSynchronize(s));
+    asr_status dst = run_decode(c, D, in->slots, in->tokens, pos, out->argmax, in->logits);
+    if (dst != ASR_OK && dst != ASR_EDEVICE) return dst;
     for (int i = 0; i < D; ++i) {
       Slot& sl2 = c->slots[in->slots[i]];
       sl2.pos += 1;
       if (sl2.steps_left > 0) sl2.steps_left -= 1;
       out->done[i] = sl2.steps_left == 0;
     }
-    if (flag) return fail(ASR_EDEVICE, "NaN logit");
+    if (dst != ASR_OK) return dst;
   }
   return collect_timing(c);
+}
+
+// ---------------------------------------------------------------------------
+// Continuous batching
+// ---------------------------------------------------------------------------
+asr_status asr_serve_config(asr_ctx* c, const asr_serve_cfg* sc) {
+  if (!c || !sc) return fail(ASR_EINVAL, "NULL argument");
+  if (!c->popped.empty()) return fail(ASR_ESTATE, "popped requests are waiting for asr_step");
+  for (const auto& sl : c->slots)
+    if (sl.occupied) return fail(ASR_ESTATE, "slots are occupied (release them first)");
+  if (c->serve.busy()) return fail(ASR_ESTATE, "requests are still being served");
+  const asr_model_cfg& g = c->cfg;
+  const int n_slots = c->device >= 0 ? std::min(g.max_slots, g.max_decode) : g.max_slots;
+  if (n_slots <= 0) return fail(ASR_EINVAL, "context has no decode slots");
+  if (sc->max_admit < 1 || (c->device >= 0 && sc->max_admit > g.max_prefill))
+    return fail(ASR_EINVAL, "max_admit out of [1, max_prefill]");
+  if (sc->cross_tokens < 0) return fail(ASR_EINVAL, "cross_tokens must be >= 0");
+  if (sc->kv_capacity > 0 && sc->kv_capacity < (int64_t)sc->cross_tokens + kTextCtx)
+    return fail(ASR_EINVAL, "kv_capacity must hold one request of 448 tokens (or be <= 0)");
+  if (sc->tok_num <= 0 || sc->tok_den <= 0) return fail(ASR_EINVAL, "token rate must be positive");
+  if (c->device >= 0 && (sc->start_token < 0 || sc->start_token >= g.vocab))
+    return fail(ASR_EINVAL, "start_token out of the vocabulary");
+  ServeConfig cfg;
+  cfg.n_slots = n_slots;
+  cfg.max_admit = sc->max_admit;
+  cfg.kv_capacity = sc->kv_capacity;
+  cfg.cross_tokens = sc->cross_tokens;
+  cfg.tok_num = sc->tok_num;
+  cfg.tok_den = sc->tok_den;
+  cfg.start_token = sc->start_token;
+  c->serve.configure(cfg);
+  c->serving.clear();
+  c->serve_mode = true;
+  return ASR_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Plan one engine step and move the request records with it.
+asr_status serve_plan_step(asr_ctx* c, int64_t now_us, const asr_serve_out* out, ServePlan* p) {
+  if (!c->serve_mode) return fail(ASR_ESTATE, "asr_serve_config has not been called");
+  if (!out || out->cap < c->serve.config().n_slots || !out->preempted || !out->admitted ||
+      !out->admitted_slot || !out->decoded || !out->token || !out->finished)
+    return fail(ASR_EINVAL, "asr_serve_out needs arrays of at least the slot count");
+  *p = c->serve.plan(now_us, c->queue);
+  for (int64_t id : p->preempted) {
+    auto it = c->serving.find(id);
+    c->waiting.emplace(id, std::move(it->second));
+    c->serving.erase(it);
+  }
+  for (int64_t id : p->admitted) {
+    auto it = c->waiting.find(id);
+    c->serving.emplace(id, std::move(it->second));
+    c->waiting.erase(it);
+  }
+  return ASR_OK;
+}
+
+void serve_finish(asr_ctx* c, const ServePlan& p, const int32_t* tokens, asr_serve_out* out) {
+  std::vector<int64_t> fin = c->serve.commit(p, tokens);
+  out->n_preempted = (int32_t)p.preempted.size();
+  for (size_t i = 0; i < p.preempted.size(); ++i) out->preempted[i] = p.preempted[i];
+  out->n_admitted = (int32_t)p.admitted.size();
+  for (size_t i = 0; i < p.admitted.size(); ++i) {
+    out->admitted[i] = p.admitted[i];
+    out->admitted_slot[i] = p.admitted_slot[i];
+  }
+  out->n_decoded = (int32_t)p.dec_id.size();
+  for (size_t i = 0; i < p.dec_id.size(); ++i) {
+    out->decoded[i] = p.dec_id[i];
+    out->token[i] = tokens ? tokens[i] : -1;
+  }
+  out->n_finished = (int32_t)fin.size();
+  for (size_t i = 0; i < fin.size(); ++i) {
+    out->finished[i] = fin[i];
+    c->serving.erase(fin[i]);
+  }
+  // mirror the engine into the slot table (asr_slot_info)
+  for (auto& sl : c->slots) sl = Slot();
+  for (size_t i = 0; i < p.dec_id.size(); ++i) {
+    const RunEntry* r = c->serve.find(p.dec_id[i]);
+    if (!r) continue;
+    Slot& sl = c->slots[r->slot];
+    sl.occupied = 1;
+    sl.id = r->q.id;
+    sl.pos = r->generated;
+    sl.steps_left = r->total - r->generated;
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+asr_status asr_serve_plan(asr_ctx* c, int64_t now_us, asr_serve_out* out) {
+  if (!c) return fail(ASR_EINVAL, "NULL context");
+  if (c->device >= 0)
+    return fail(ASR_ESTATE, "asr_serve_plan runs the schedule without the model: queue-only contexts");
+  ServePlan p;
+  asr_status st = serve_plan_step(c, now_us, out, &p);
+  if (st != ASR_OK) return st;
+  serve_finish(c, p, nullptr, out);
+  return ASR_OK;
+}
+
+asr_status asr_serve_step(asr_ctx* c, int64_t now_us, asr_serve_out* out) {
+  asr_status st = need_gpu(c, true);
+  if (st != ASR_OK) return st;
+  if (c->cfg.n_enc == 0 || c->cfg.n_dec == 0)
+    return fail(ASR_EINVAL, "continuous batching needs an encoder and a decoder");
+  ServePlan p;
+  st = serve_plan_step(c, now_us, out, &p);
+  if (st != ASR_OK) return st;
+  HIPCHK(hipSetDevice(c->device));
+  std::vector<const Request*> reqs;
+  for (int64_t id : p.admitted) {
+    const Request& r = c->serving.at(id);
+    if (!r.has_audio) return fail(ASR_EINVAL, "request " + std::to_string(id) + " has no samples");
+    reqs.push_back(&r);
+  }
+  st = run_prefill(c, reqs, p.admitted_slot);
+  if (st != ASR_OK) return st;
+  const int D = (int)p.dec_id.size();
+  std::vector<int32_t> tok(D);
+  st = run_decode(c, D, p.dec_slot.data(), p.dec_token.data(), p.dec_pos, tok.data(), nullptr);
+  if (st != ASR_OK) return st;
+  serve_finish(c, p, tok.data(), out);
+  return collect_timing(c);
+}
+
+asr_status asr_serve_simulate(asr_ctx* c, const asr_sim_cost* cost, int64_t t0_us, int32_t n,
+                              const int64_t* ids, int64_t* first_us, int64_t* finish_us,
+                              int32_t* n_tokens, int32_t* n_preempt, int64_t* token_us,
+                              int64_t token_cap, int64_t* t_end_us) {
+  if (!c || !cost || (n > 0 && (!ids || !first_us || !finish_us || !n_tokens || !n_preempt)) ||
+      !t_end_us)
+    return fail(ASR_EINVAL, "NULL argument");
+  if (c->device >= 0) return fail(ASR_ESTATE, "simulations run on queue-only contexts");
+  if (!c->serve_mode) return fail(ASR_ESTATE, "asr_serve_config has not been called");
+  if (cost->prefill_us < 0 || cost->step_us < 0 || cost->row_us < 0 ||
+      cost->prefill_us + cost->step_us + cost->row_us <= 0)
+    return fail(ASR_EINVAL, "step costs must be >= 0 and not all zero");
+  if (c->serve.busy()) return fail(ASR_ESTATE, "requests are already being served");
+  if ((size_t)n != c->waiting.size()) return fail(ASR_EINVAL, "ids must list every submitted request");
+  std::unordered_map<int64_t, int32_t> idx;
+  int64_t off = 0;
+  std::vector<int64_t> tok_off(n);
+  for (int32_t i = 0; i < n; ++i) {
+    auto it = c->waiting.find(ids[i]);
+    if (it == c->waiting.end() || idx.count(ids[i]))
+      return fail(ASR_EINVAL, "id " + std::to_string(ids[i]) + " is not a distinct waiting request");
+    idx[ids[i]] = i;
+    const Request& r = it->second;
+    QEntry e{r.id, r.arrival_us, r.n_samples, r.dur_us, r.sample_rate, r.max_tokens, 0};
+    tok_off[i] = off;
+    off += c->serve.tokens_for(e);
+    first_us[i] = finish_us[i] = -1;
+    n_tokens[i] = n_preempt[i] = 0;
+  }
+  if (token_us && token_cap < off) return fail(ASR_EINVAL, "token_us needs room for every token");
+  int64_t t = t0_us;
+  int32_t left = n;
+  asr_serve_out dummy{};
+  std::vector<int32_t> gen;
+  while (left > 0) {
+    if (!c->serve.busy() && !c->queue.any_eligible(t)) {
+      t = c->queue.min_arrival();
+      continue;
+    }
+    ServePlan p = c->serve.plan(t, c->queue);
+    for (int64_t id : p.preempted) {
+      auto it = c->serving.find(id);
+      c->waiting.emplace(id, std::move(it->second));
+      c->serving.erase(it);
+      n_preempt[idx[id]] += 1;
+    }
+    for (int64_t id : p.admitted) {
+      auto it = c->waiting.find(id);
+      c->serving.emplace(id, std::move(it->second));
+      c->waiting.erase(it);
+    }
+    const int64_t nd = (int64_t)p.dec_id.size();
+    t += cost->prefill_us * (int64_t)p.admitted.size() +
+         (nd > 0 ? cost->step_us + cost->row_us * nd : 0);
+    std::vector<int64_t> fin = c->serve.commit(p, nullptr, &gen);
+    for (size_t i = 0; i < p.dec_id.size(); ++i) {
+      const int32_t k = idx[p.dec_id[i]];
+      // a position that a recomputed request reaches again is not emitted again
+      while (n_tokens[k] < gen[i]) {
+        if (token_us) token_us[tok_off[k] + n_tokens[k]] = t;
+        if (n_tokens[k] == 0) first_us[k] = t;
+        n_tokens[k] += 1;
+      }
+    }
+    for (int64_t id : fin) {
+      finish_us[idx[id]] = t;
+      c->serving.erase(id);
+      (void)c->serve.take_result(id, nullptr);
+      --left;
+    }
+    (void)dummy;
+  }
+  *t_end_us = t;
+  return ASR_OK;
+}
+
+asr_status asr_serve_tokens(asr_ctx* c, int64_t id, int32_t* tokens, int32_t cap, int32_t* n) {
+  if (!c || !n || (cap > 0 && !tokens)) return fail(ASR_EINVAL, "NULL argument");
+  std::vector<int32_t> t;
+  if (!c->serve.take_result(id, &t)) return fail(ASR_ENOTFOUND, "no finished request " + std::to_string(id));
+  if ((int32_t)t.size() > cap) return fail(ASR_EINVAL, "token buffer too small");
+  for (size_t i = 0; i < t.size(); ++i) tokens[i] = t[i];
+  *n = (int32_t)t.size();
+  return ASR_OK;
 }
 
 asr_status asr_set_timing(asr_ctx* c, int32_t classes) {
