@@ -221,8 +221,10 @@ typedef enum {
  * running request holds cross_tokens plus one per generated token.
  * ------------------------------------------------------------------------- */
 typedef struct {
-  int64_t kv_capacity;  /* pool size in token positions; <= 0: slots are the only bound;
-                           otherwise >= cross_tokens + 448 */
+  int64_t kv_capacity;  /* pool size in token positions; <= 0: slots are the only bound.
+                           Every request must fit on its own (cross_tokens + its token
+                           count): asr_serve_config and later asr_submit calls reject
+                           one that cannot (EINVAL), since it could never finish */
   int32_t cross_tokens; /* positions charged for a request's cross cache (1500) */
   int32_t max_admit;    /* admissions per step, 1 .. max_prefill */
   int32_t tok_num;      /* output tokens per audio-second = tok_num / tok_den (27/10) */

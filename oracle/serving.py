@@ -21,7 +21,9 @@ Readings where the paper is silent (the same ones the engine takes):
   running request grows by one position per step;
 * a preempted request drops its tokens, keeps its arrival time and keys, and
   is not re-admitted in the step that evicted it;
-* admission stops at the first request the pool cannot hold;
+* admission stops at the first request the pool cannot hold; a request that
+  could not fit the pool even alone is refused at submission (it could never
+  finish);
 * an admitted request is prefilled and produces its first token in the step
   that admits it;
 * tokens per request: round-half-up(duration * rate), clamped to
@@ -98,6 +100,10 @@ class Engine:
         self.queue = Q.Queue(self.policy, self.kappa_num, self.kappa_den)
 
     def submit(self, rid, n_samples, sample_rate, arrival_us, duration_us=0, max_tokens=0):
+        mt = max_tokens if max_tokens > 0 else Q.MAX_TOKENS
+        need = self.cross_tokens + tokens_for(n_samples, sample_rate, mt, self.tok_num, self.tok_den)
+        if self.kv_capacity > 0 and need > self.kv_capacity:
+            raise ValueError(f"request {rid} can never fit the KV pool")
         self.queue.submit(rid, n_samples, sample_rate, arrival_us, duration_us, max_tokens)
         self.known[rid] = self.queue.reqs[rid]
 

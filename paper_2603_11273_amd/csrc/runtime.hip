@@ -954,6 +954,11 @@ asr_status asr_submit(asr_ctx* c, int64_t id, const float* pcm, int64_t n_sample
       r.pcm.assign(pcm, pcm + n_samples);
   }
   QEntry e{id, r.arrival_us, r.n_samples, r.dur_us, r.sample_rate, r.max_tokens, 0};
+  if (c->serve_mode) {
+    const ServeConfig& sc = c->serve.config();
+    if (sc.kv_capacity > 0 && (int64_t)sc.cross_tokens + c->serve.tokens_for(e) > sc.kv_capacity)
+      return fail(ASR_EINVAL, "request can never fit the KV pool (cross share + its tokens)");
+  }
   c->queue.push(e);
   c->waiting.emplace(id, std::move(r));
   return ASR_OK;
@@ -1169,12 +1174,23 @@ asr_status asr_serve_config(asr_ctx* c, const asr_serve_cfg* sc) {
   if (sc->max_admit < 1 || (c->device >= 0 && sc->max_admit > g.max_prefill))
     return fail(ASR_EINVAL, "max_admit out of [1, max_prefill]");
   if (sc->cross_tokens < 0) return fail(ASR_EINVAL, "cross_tokens must be >= 0");
-  if (sc->kv_capacity > 0 && sc->kv_capacity < (int64_t)sc->cross_tokens + kTextCtx)
-    return fail(ASR_EINVAL, "kv_capacity must hold one request of 448 tokens (or be <= 0)");
   if (sc->tok_num <= 0 || sc->tok_den <= 0) return fail(ASR_EINVAL, "token rate must be positive");
   if (c->device >= 0 && (sc->start_token < 0 || sc->start_token >= g.vocab))
     return fail(ASR_EINVAL, "start_token out of the vocabulary");
   ServeConfig cfg;
+  cfg.tok_num = sc->tok_num;
+  cfg.tok_den = sc->tok_den;
+  if (sc->kv_capacity > 0) {
+    // every request must fit the pool on its own, or it could never finish
+    ServeEngine probe;
+    probe.configure(cfg);
+    for (const auto& kv : c->waiting) {
+      const Request& r = kv.second;
+      QEntry e{r.id, r.arrival_us, r.n_samples, r.dur_us, r.sample_rate, r.max_tokens, 0};
+      if ((int64_t)sc->cross_tokens + probe.tokens_for(e) > sc->kv_capacity)
+        return fail(ASR_EINVAL, "request " + std::to_string(r.id) + " can never fit the KV pool");
+    }
+  }
   cfg.n_slots = n_slots;
   cfg.max_admit = sc->max_admit;
   cfg.kv_capacity = sc->kv_capacity;

@@ -70,34 +70,33 @@ def test_oracle_token_counts():
 
 
 def test_oracle_preemption_rule_by_hand():
-    """Hand-built pressure: A (6 s, arrives at 0 us), B (2 s, at 1 us), C
-    (4 s, at 2 us); 10 tokens per audio-second (60, 20, 40 tokens), cross
-    share 10 positions, pool 48, one admission per step, steps at t = 0, 1,
-    2, ... us.  Before the step at t >= 2 the three hold t, t-1, t-2 tokens,
-    so the step needs 3*10 + (t+1) + t + (t-1) = 30 + 3t positions: first
-    above 48 at t = 7, where exactly one request must go.  SJF evicts the
-    longest job (A), FCFS the last admitted (C), HRRN the lowest
-    (wait + job) / job -- A, with the ratios written out below."""
+    """Hand-built pressure: A (3 s, arrives at 0 us), B (1 s, at 1 us), C
+    (2 s, at 2 us); 10 tokens per audio-second (30, 10, 20 tokens; each fits
+    the pool alone), cross share 4 positions, pool 40, one admission per step,
+    steps at t = 0, 1, 2, ... us.  Before the step at t >= 2 the three hold t,
+    t-1, t-2 tokens (B, with 10, is still running at t = 10), so the step
+    needs 3*4 + (t+1) + t + (t-1) = 12 + 3t positions: first above 40 at
+    t = 10, where exactly one request must go (evicting any one brings the
+    need to at most 28).  SJF evicts the longest job (A), FCFS the last
+    admitted (C), HRRN the lowest (wait + job) / job -- A, with the ratios
+    written out below."""
     def run(policy):
-        eng = S.Engine(policy, n_slots=3, max_admit=1, kv_capacity=48, cross_tokens=10,
+        eng = S.Engine(policy, n_slots=3, max_admit=1, kv_capacity=40, cross_tokens=4,
                        tok_num=10, tok_den=1)
-        eng.submit(1, 6 * SR, SR, 0)        # 60 tokens
-        eng.submit(2, 2 * SR, SR, 1)        # 20 tokens
-        eng.submit(3, 4 * SR, SR, 2)        # 40 tokens
-        for t in range(10):
+        eng.submit(1, 3 * SR, SR, 0)        # 30 tokens
+        eng.submit(2, 1 * SR, SR, 1)        # 10 tokens
+        eng.submit(3, 2 * SR, SR, 2)        # 20 tokens
+        for t in range(12):
             res = eng.step(t)
             if res.preempted:
                 return t, res.preempted
         return None
-    # need at step t (all three running, admitted at 0, 1, 2): generated before the
-    # step = t, t-1, t-2 -> need = 3*10 + (t+1) + t + (t-1) = 30 + 3t > 48 first at t = 7
-    assert run(Q.SJF) == (7, [1])           # largest job: A (60 tokens)
-    assert run(Q.FCFS) == (7, [3])          # last admitted: C
-    # HRRN at t = 7 us: ratios (w + e) / e with e = duration in us
-    r = {1: Fraction(7 + 6_000_000, 6_000_000), 2: Fraction(6 + 2_000_000, 2_000_000),
-         3: Fraction(5 + 4_000_000, 4_000_000)}
-    lowest = min(r, key=lambda k: r[k])
-    assert lowest == 1 and run(Q.HRRN) == (7, [1])
+    assert run(Q.SJF) == (10, [1])          # largest job: A
+    assert run(Q.FCFS) == (10, [3])         # last admitted: C
+    # HRRN at t = 10 us: ratios (w + e) / e with e = duration in us
+    r = {1: Fraction(10 + 3_000_000, 3_000_000), 2: Fraction(9 + 1_000_000, 1_000_000),
+         3: Fraction(8 + 2_000_000, 2_000_000)}
+    assert min(r, key=lambda k: r[k]) == 1 and run(Q.HRRN) == (10, [1])
 
 
 def test_oracle_pool_never_exceeded_and_all_finish():
@@ -213,9 +212,14 @@ def test_native_rejects_misuse():
         c.pop_batch(0, 1)                     # manual API is off in serve mode
     with pytest.raises(asr.AsrError):
         c.serve_tokens(99)                    # unknown request
+    c3 = _ctx(asr.SJF, n_slots=4, kv_capacity=1550, cross_tokens=1500)
+    c3.submit(1, None, n_samples=30 * SR // 10)          # 8 tokens: fits
+    with pytest.raises(asr.AsrError):
+        c3.submit(2, None, n_samples=30 * SR)            # 81 tokens + 1500 > 1550
     cfg = asr.model_cfg(synth.SHAPES["tiny"], max_slots=4, max_prefill=1, max_decode=4)
     c2 = asr.Context(cfg, device=-1)
+    c2.submit(7, None, n_samples=30 * SR)
     with pytest.raises(asr.AsrError):
-        c2.serve_config(kv_capacity=100, cross_tokens=1500)   # pool below one request
+        c2.serve_config(kv_capacity=1550, cross_tokens=1500)   # a waiting request cannot fit
     with pytest.raises(asr.AsrError):
         c2.serve_plan(0)                      # not configured
