@@ -24,7 +24,26 @@ bool WaitQueue::before(const QEntry& a, const QEntry& b, int64_t now_us) const {
   return a.id < b.id;
 }
 
+namespace {
+bool arrives_after(const QEntry& x, const QEntry& y) {
+  if (x.arrival_us != y.arrival_us) return x.arrival_us > y.arrival_us;
+  return x.id > y.id;
+}
+}  // namespace
+
+void WaitQueue::admit_arrived(int64_t now_us) {
+  auto cmp = [this](const QEntry& x, const QEntry& y) { return before(y, x, 0); };
+  while (!later_.empty() && later_.front().arrival_us <= now_us) {
+    std::pop_heap(later_.begin(), later_.end(), arrives_after);
+    items_.push_back(later_.back());
+    later_.pop_back();
+    std::push_heap(items_.begin(), items_.end(), cmp);
+  }
+}
+
 void WaitQueue::rebuild() {
+  for (auto& e : later_) items_.push_back(e);
+  later_.clear();
   for (auto& e : items_) e.job = job_of(e);
   if (policy_ != HRRN)
     std::make_heap(items_.begin(), items_.end(),
@@ -41,16 +60,20 @@ void WaitQueue::set_policy(int policy, int32_t kappa_num, int32_t kappa_den) {
 void WaitQueue::push(QEntry e) {
   e.job = job_of(e);
   ids_.insert(e.id);
-  items_.push_back(e);
-  if (policy_ != HRRN)
-    std::push_heap(items_.begin(), items_.end(),
-                   [this](const QEntry& x, const QEntry& y) { return before(y, x, 0); });
+  if (policy_ == HRRN) {
+    items_.push_back(e);
+  } else {
+    later_.push_back(e);
+    std::push_heap(later_.begin(), later_.end(), arrives_after);
+  }
 }
 
 std::vector<int64_t> WaitQueue::rank(int64_t now_us) const {
   std::vector<const QEntry*> el;
-  el.reserve(items_.size());
+  el.reserve(size());
   for (const auto& e : items_)
+    if (e.arrival_us <= now_us) el.push_back(&e);
+  for (const auto& e : later_)
     if (e.arrival_us <= now_us) el.push_back(&e);
   std::sort(el.begin(), el.end(),
             [&](const QEntry* x, const QEntry* y) { return before(*x, *y, now_us); });
@@ -77,8 +100,9 @@ std::vector<QEntry> WaitQueue::pop_batch(int64_t now_us, int max_n) {
       items_.pop_back();
     }
   } else {
+    admit_arrived(now_us);
     auto cmp = [this](const QEntry& x, const QEntry& y) { return before(y, x, 0); };
-    std::vector<QEntry> later;                 // popped but not yet arrived
+    std::vector<QEntry> later;                 // popped but not yet arrived (an earlier now)
     while ((int)out.size() < max_n && !items_.empty()) {
       std::pop_heap(items_.begin(), items_.end(), cmp);
       QEntry e = items_.back();
@@ -100,13 +124,14 @@ std::vector<QEntry> WaitQueue::pop_batch(int64_t now_us, int max_n) {
 }
 
 bool WaitQueue::any_eligible(int64_t now_us) const {
+  if (!later_.empty() && later_.front().arrival_us <= now_us) return true;
   for (const auto& e : items_)
     if (e.arrival_us <= now_us) return true;
   return false;
 }
 
 int64_t WaitQueue::min_arrival() const {
-  int64_t m = INT64_MAX;
+  int64_t m = later_.empty() ? INT64_MAX : later_.front().arrival_us;
   for (const auto& e : items_) m = std::min(m, e.arrival_us);
   return m;
 }

@@ -41,7 +41,7 @@ class WaitQueue {
   void set_policy(int policy, int32_t kappa_num, int32_t kappa_den);
   int policy() const { return policy_; }
   bool contains(int64_t id) const { return ids_.count(id) != 0; }
-  size_t size() const { return items_.size(); }
+  size_t size() const { return items_.size() + later_.size(); }
   void push(QEntry e);
   std::vector<int64_t> rank(int64_t now_us) const;
   std::vector<QEntry> pop_batch(int64_t now_us, int max_n);
@@ -53,9 +53,16 @@ class WaitQueue {
   bool before(const QEntry& a, const QEntry& b, int64_t now_us) const;
   void rebuild();
 
+  // FCFS/SJF keep requests that may not have arrived yet in a separate heap
+  // by arrival time and move them into the policy heap once a pop sees their
+  // arrival, so a queue holding many future requests (a simulation submits
+  // them all up front) still pops in logarithmic time.
+  void admit_arrived(int64_t now_us);
+
   int policy_ = FCFS;
   int32_t kn_ = 0, kd_ = 0;
   std::vector<QEntry> items_;   // binary heap under FCFS/SJF, plain list under HRRN
+  std::vector<QEntry> later_;   // FCFS/SJF: min-heap by (arrival, id), not yet moved
   std::unordered_set<int64_t> ids_;
 };
 
