@@ -347,11 +347,19 @@ def serving_section(ctx, D, P, enc_ms, dec_ms, toks, steps_done):
     log(f"GPU burst: {gpu}")
 
     # 3. the paper's evaluation on the virtual clock
+    DYNAMIC = 3
+
     def run(policy, n, rate, burst=False):
         q = asr.Context(asr.model_cfg(synth.SHAPES["large-v3"], max_slots=D, max_prefill=P,
                                       max_decode=D, max_queue=n + 1), device=-1)
-        q.set_policy(policy)
-        q.serve_config(kv_capacity=0, cross_tokens=1500, max_admit=P)
+        if policy == DYNAMIC:
+            # FCFS while every eligible request is admitted this step, HRRN once
+            # some request's response ratio passes 3, SJF otherwise
+            q.serve_config(kv_capacity=0, cross_tokens=1500, max_admit=P, dynamic=True,
+                           depth_low=P, starve=(3, 1))
+        else:
+            q.set_policy(policy)
+            q.serve_config(kv_capacity=0, cross_tokens=1500, max_admit=P)
         s2 = seed + int(rate * 10)
         n_s = synth.n_samples_of(synth.durations_lognormal(s2, n))
         arr = np.zeros(n, np.int64) if burst else synth.poisson_arrivals_us(s2, n, rate)
@@ -363,12 +371,16 @@ def serving_section(ctx, D, P, enc_ms, dec_ms, toks, steps_done):
         ttft = np.array([info[i]["first_us"] - arr[i] for i in range(n)]) * 1e-6
         e2el = np.array([info[i]["finish_us"] - arr[i] for i in range(n)]) * 1e-6
         pct = lambda v, p: float(np.percentile(v, p, method="inverted_cdf"))  # noqa: E731
-        return {"ttft_p50_s": round(pct(ttft, 50), 3), "ttft_p90_s": round(pct(ttft, 90), 3),
+        extra = {}
+        if policy == DYNAMIC:
+            st = q.serve_stats()
+            extra["steps_fcfs_sjf_hrrn"] = st
+        return {**extra, "ttft_p50_s": round(pct(ttft, 50), 3), "ttft_p90_s": round(pct(ttft, 90), 3),
                 "e2el_p50_s": round(pct(e2el, 50), 3), "e2el_p90_s": round(pct(e2el, 90), 3),
                 "req_per_s": round(n / ((t_end - int(arr.min())) * 1e-6), 2),
                 "sched_host_us_per_request": round(host_us, 2)}
 
-    names = {asr.FCFS: "fcfs", asr.SJF: "sjf", asr.HRRN: "hrrn"}
+    names = {asr.FCFS: "fcfs", asr.SJF: "sjf", asr.HRRN: "hrrn", DYNAMIC: "dynamic"}
     sim = {"burst_500": {names[p]: run(p, 500, 0, burst=True) for p in names}}
     # Poisson streams (60 s each) at fractions of the engine's saturation rate
     # (the burst's throughput): the paper's 1-25 req/s span the A100 engine's
@@ -380,7 +392,7 @@ def serving_section(ctx, D, P, enc_ms, dec_ms, toks, steps_done):
             rate_per_s=rate, **{names[p]: run(p, int(rate * 60), rate) for p in names})
     for case in sim.values():
         base = case["fcfs"]
-        for pol in ("sjf", "hrrn"):
+        for pol in ("sjf", "hrrn", "dynamic"):
             case[pol]["vs_fcfs_pct"] = {
                 k: round(100.0 * (case[pol][k] - base[k]) / base[k], 1) if base[k] else None
                 for k in ("ttft_p50_s", "ttft_p90_s", "e2el_p50_s", "e2el_p90_s")}

@@ -230,12 +230,24 @@ typedef struct {
   int32_t tok_num;      /* output tokens per audio-second = tok_num / tok_den (27/10) */
   int32_t tok_den;
   int32_t start_token;  /* decoder input at position 0 */
+  /* Dynamic policy switching (the future-work paragraph of Section 5: watch
+   * the queue and switch among FCFS, SJF and HRRN).  0: the policy of
+   * asr_set_policy throughout.  1: at the start of every step, FCFS while at
+   * most depth_low requests are eligible (they all get in anyway); otherwise
+   * HRRN when some eligible request's response ratio (wait + job) / job
+   * exceeds starve_num / starve_den (a starvation signal), else SJF.  The
+   * chosen policy orders that step's admissions and picks its victims. */
+  int32_t dynamic;
+  int32_t depth_low;
+  int64_t starve_num;
+  int64_t starve_den;   /* > 0 when dynamic */
 } asr_serve_cfg;
 
 /* Arrays are the caller's, each with room for cap >= the slot count
  * (min(max_slots, max_decode) on a GPU context, max_slots queue-only). */
 typedef struct {
   int32_t cap;
+  int32_t policy;         /* policy the step ran under (asr_policy) */
   int64_t* preempted;     int32_t n_preempted;
   int64_t* admitted;      int32_t* admitted_slot;  int32_t n_admitted;
   int64_t* decoded;       int32_t* token;          int32_t n_decoded;  /* token -1: no model ran */
@@ -252,6 +264,8 @@ asr_status asr_serve_step(asr_ctx* ctx, int64_t now_us, asr_serve_out* out);
 /* The same schedule without running the model (tokens -1), for queue-only
  * contexts (device = -1; ESTATE otherwise): simulations and CPU tests. */
 asr_status asr_serve_plan(asr_ctx* ctx, int64_t now_us, asr_serve_out* out);
+/* Steps run under each policy since asr_serve_config (steps[ASR_FCFS] ..). */
+asr_status asr_serve_stats(const asr_ctx* ctx, int64_t steps[3]);
 /* Tokens of a finished request, once (ENOTFOUND otherwise; EINVAL when cap is
  * smaller than the token count). */
 asr_status asr_serve_tokens(asr_ctx* ctx, int64_t id, int32_t* tokens, int32_t cap, int32_t* n);

@@ -37,6 +37,7 @@ oracle can be compared event for event.
 from __future__ import annotations
 
 from dataclasses import dataclass, field
+from fractions import Fraction
 
 from . import queue as Q
 
@@ -73,11 +74,27 @@ def victim_key(r: Running, policy: int, now_us: int):
 
 @dataclass
 class StepResult:
+    policy: int
     preempted: list
     admitted: list            # (id, slot)
     decoded: list             # ids, in decode-row order
     generated: dict           # id -> tokens held after the step
     finished: list
+
+
+def dynamic_policy(waiting, now_us, depth_low, starve, kappa_num=0, kappa_den=0):
+    """Dynamic switching (Section 5, future work: watch queue depth and
+    starvation, switch among FCFS, SJF and HRRN) as this build reads it:
+    FCFS while at most depth_low requests are eligible (all of them are about
+    to be admitted, so the order costs nothing); otherwise HRRN when some
+    eligible request's response ratio exceeds `starve` (a Fraction), else
+    SJF."""
+    elig = [r for r in waiting if r.arrival_us <= now_us]
+    if len(elig) <= depth_low:
+        return Q.FCFS
+    top = max(Q.response_ratio(now_us - r.arrival_us, Q.job_length(r, kappa_num, kappa_den))
+              for r in elig)
+    return Q.HRRN if top > starve else Q.SJF
 
 
 @dataclass
@@ -91,10 +108,14 @@ class Engine:
     tok_den: int = 10
     kappa_num: int = 0
     kappa_den: int = 0
+    dynamic: bool = False
+    depth_low: int = 0
+    starve: Fraction = Fraction(0)
     queue: Q.Queue = None
     known: dict = field(default_factory=dict)
     running: list = field(default_factory=list)
     seq: int = 0
+    steps_by_policy: list = field(default_factory=lambda: [0, 0, 0])
 
     def __post_init__(self):
         self.queue = Q.Queue(self.policy, self.kappa_num, self.kappa_den)
@@ -112,6 +133,11 @@ class Engine:
         return tokens_for(r.n_samples, r.sample_rate, r.max_tokens, self.tok_num, self.tok_den)
 
     def step(self, now_us: int) -> StepResult:
+        if self.dynamic:
+            self.policy = dynamic_policy(self.queue.reqs.values(), now_us, self.depth_low,
+                                         self.starve, self.kappa_num, self.kappa_den)
+            self.queue.policy = self.policy
+        self.steps_by_policy[self.policy] += 1
         limited = self.kv_capacity > 0
         need = sum(self.cross_tokens + r.generated + 1 for r in self.running)
         preempted, requeue = [], []
@@ -147,7 +173,7 @@ class Engine:
             if r.generated >= r.total:
                 self.running.remove(r)
                 finished.append(r.req.rid)
-        return StepResult(preempted, admitted, decoded, generated, finished)
+        return StepResult(self.policy, preempted, admitted, decoded, generated, finished)
 
 
 @dataclass

@@ -30,7 +30,7 @@ EXPORTED = [
     "asr_slot_info", "asr_set_timing", "asr_get_timing", "asr_reset_timing",
     "asr_debug_logmel", "asr_debug_encode", "asr_debug_set_encoder_out", "asr_debug_get_kv",
     "asr_debug_set_self_kv", "asr_serve_config", "asr_serve_step", "asr_serve_plan",
-    "asr_serve_tokens", "asr_serve_simulate",
+    "asr_serve_tokens", "asr_serve_simulate", "asr_serve_stats",
 ]
 
 
@@ -54,11 +54,12 @@ class StepOut(C.Structure):
 class ServeCfg(C.Structure):
     _fields_ = [("kv_capacity", C.c_int64), ("cross_tokens", C.c_int32),
                 ("max_admit", C.c_int32), ("tok_num", C.c_int32), ("tok_den", C.c_int32),
-                ("start_token", C.c_int32)]
+                ("start_token", C.c_int32), ("dynamic", C.c_int32), ("depth_low", C.c_int32),
+                ("starve_num", C.c_int64), ("starve_den", C.c_int64)]
 
 
 class ServeOut(C.Structure):
-    _fields_ = [("cap", C.c_int32),
+    _fields_ = [("cap", C.c_int32), ("policy", C.c_int32),
                 ("preempted", C.POINTER(C.c_int64)), ("n_preempted", C.c_int32),
                 ("admitted", C.POINTER(C.c_int64)), ("admitted_slot", C.POINTER(C.c_int32)),
                 ("n_admitted", C.c_int32),
@@ -120,6 +121,7 @@ def _load():
         "asr_serve_step": [vp, i64, P(ServeOut)],
         "asr_serve_plan": [vp, i64, P(ServeOut)],
         "asr_serve_tokens": [vp, i64, P(i32), i32, P(i32)],
+        "asr_serve_stats": [vp, P(i64)],
         "asr_serve_simulate": [vp, P(SimCost), i64, i32, P(i64), P(i64), P(i64), P(i32),
                                P(i32), P(i64), i64, P(i64)],
     }
@@ -281,8 +283,10 @@ class Context:
 
     # -- continuous batching ----------------------------------------------------
     def serve_config(self, kv_capacity=0, cross_tokens=1500, max_admit=1, tok_num=27,
-                     tok_den=10, start_token=0):
-        cfg = ServeCfg(kv_capacity, cross_tokens, max_admit, tok_num, tok_den, start_token)
+                     tok_den=10, start_token=0, dynamic=False, depth_low=0, starve=(0, 1)):
+        """starve = (num, den): the response-ratio threshold of the dynamic rule."""
+        cfg = ServeCfg(kv_capacity, cross_tokens, max_admit, tok_num, tok_den, start_token,
+                       int(dynamic), depth_low, starve[0], starve[1])
         _check(lib.asr_serve_config(self.h, C.byref(cfg)))
         self._serve_cap = max(self.cfg.max_slots, 1)
 
@@ -293,10 +297,11 @@ class Context:
         tok = np.zeros(cap, np.int32)
         p64 = lambda a: a.ctypes.data_as(C.POINTER(C.c_int64))  # noqa: E731
         p32 = lambda a: a.ctypes.data_as(C.POINTER(C.c_int32))  # noqa: E731
-        out = ServeOut(cap, p64(bufs["preempted"]), 0, p64(bufs["admitted"]), p32(slot), 0,
+        out = ServeOut(cap, 0, p64(bufs["preempted"]), 0, p64(bufs["admitted"]), p32(slot), 0,
                        p64(bufs["decoded"]), p32(tok), 0, p64(bufs["finished"]), 0)
         _check(fn(self.h, now_us, C.byref(out)))
-        return {"preempted": bufs["preempted"][:out.n_preempted].tolist(),
+        return {"policy": out.policy,
+                "preempted": bufs["preempted"][:out.n_preempted].tolist(),
                 "admitted": bufs["admitted"][:out.n_admitted].tolist(),
                 "admitted_slot": slot[:out.n_admitted].tolist(),
                 "decoded": bufs["decoded"][:out.n_decoded].tolist(),
@@ -339,6 +344,12 @@ class Context:
                              "token_us": tok[off:off + k].tolist() if tok is not None else None}
             off += k
         return out, t_end.value
+
+    def serve_stats(self):
+        """Steps run under FCFS, SJF and HRRN since serve_config."""
+        a = (C.c_int64 * 3)()
+        _check(lib.asr_serve_stats(self.h, a))
+        return list(a)
 
     def serve_tokens(self, rid):
         buf = np.zeros(448, np.int32)

@@ -136,4 +136,27 @@ int64_t WaitQueue::min_arrival() const {
   return m;
 }
 
+int WaitQueue::eligible_count(int64_t now_us) const {
+  int n = 0;
+  for (const auto& e : items_) n += e.arrival_us <= now_us;
+  for (const auto& e : later_) n += e.arrival_us <= now_us;
+  return n;
+}
+
+void WaitQueue::max_ratio(int64_t now_us, int64_t* num, int64_t* den) const {
+  int64_t bn = 0, bd = 1;
+  auto visit = [&](const QEntry& e) {
+    if (e.arrival_us > now_us) return;
+    const int64_t n = now_us - e.arrival_us + e.job, d = e.job;
+    if ((__int128)n * bd > (__int128)bn * d) {
+      bn = n;
+      bd = d;
+    }
+  };
+  for (const auto& e : items_) visit(e);
+  for (const auto& e : later_) visit(e);
+  *num = bn;
+  *den = bd;
+}
+
 }  // namespace asr

@@ -40,6 +40,12 @@ class WaitQueue {
   // or max_tokens when the request carries no samples.
   void set_policy(int policy, int32_t kappa_num, int32_t kappa_den);
   int policy() const { return policy_; }
+  int32_t kappa_num() const { return kn_; }
+  int32_t kappa_den() const { return kd_; }
+  // Eligible requests (arrival <= now) and, over them, the largest HRRN
+  // response ratio as a fraction (wait + job) / job (0/1 when none).
+  int eligible_count(int64_t now_us) const;
+  void max_ratio(int64_t now_us, int64_t* num, int64_t* den) const;
   bool contains(int64_t id) const { return ids_.count(id) != 0; }
   size_t size() const { return items_.size() + later_.size(); }
   void push(QEntry e);

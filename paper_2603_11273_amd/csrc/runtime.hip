@@ -1191,6 +1191,12 @@ asr_status asr_serve_config(asr_ctx* c, const asr_serve_cfg* sc) {
         return fail(ASR_EINVAL, "request " + std::to_string(r.id) + " can never fit the KV pool");
     }
   }
+  if (sc->dynamic && (sc->depth_low < 0 || sc->starve_num < 0 || sc->starve_den <= 0))
+    return fail(ASR_EINVAL, "dynamic policy: depth_low >= 0, starve_num >= 0, starve_den > 0");
+  cfg.dynamic = sc->dynamic != 0;
+  cfg.depth_low = sc->depth_low;
+  cfg.starve_num = sc->starve_num;
+  cfg.starve_den = sc->dynamic ? sc->starve_den : 1;
   cfg.n_slots = n_slots;
   cfg.max_admit = sc->max_admit;
   cfg.kv_capacity = sc->kv_capacity;
@@ -1230,6 +1236,7 @@ asr_status serve_plan_step(asr_ctx* c, int64_t now_us, const asr_serve_out* out,
 
 void serve_finish(asr_ctx* c, const ServePlan& p, const int32_t* tokens, asr_serve_out* out) {
   std::vector<int64_t> fin = c->serve.commit(p, tokens);
+  out->policy = p.policy;
   out->n_preempted = (int32_t)p.preempted.size();
   for (size_t i = 0; i < p.preempted.size(); ++i) out->preempted[i] = p.preempted[i];
   out->n_admitted = (int32_t)p.admitted.size();
@@ -1373,6 +1380,12 @@ asr_status asr_serve_simulate(asr_ctx* c, const asr_sim_cost* cost, int64_t t0_u
     (void)dummy;
   }
   *t_end_us = t;
+  return ASR_OK;
+}
+
+asr_status asr_serve_stats(const asr_ctx* c, int64_t steps[3]) {
+  if (!c || !steps) return fail(ASR_EINVAL, "NULL argument");
+  for (int k = 0; k < 3; ++k) steps[k] = c->serve.steps_under(k);
   return ASR_OK;
 }
 

@@ -11,6 +11,7 @@ void ServeEngine::configure(const ServeConfig& c) {
   seq_ = 0;
   free_slots_.clear();
   for (int s = 0; s < cfg_.n_slots; ++s) free_slots_.push_back(s);
+  steps_by_policy_[0] = steps_by_policy_[1] = steps_by_policy_[2] = 0;
 }
 
 int64_t ServeEngine::kv_used() const {
@@ -46,9 +47,24 @@ bool ServeEngine::worse(const RunEntry& a, const RunEntry& b, int64_t now_us, in
   return a.q.id > b.q.id;
 }
 
+int ServeEngine::choose_policy(int64_t now_us, const WaitQueue& q) const {
+  if (q.eligible_count(now_us) <= cfg_.depth_low) return WaitQueue::FCFS;
+  int64_t n = 0, d = 1;
+  q.max_ratio(now_us, &n, &d);
+  // n / d > starve_num / starve_den
+  if ((__int128)n * cfg_.starve_den > (__int128)cfg_.starve_num * d) return WaitQueue::HRRN;
+  return WaitQueue::SJF;
+}
+
 ServePlan ServeEngine::plan(int64_t now_us, WaitQueue& q) {
   ServePlan p;
+  if (cfg_.dynamic) {
+    const int want = choose_policy(now_us, q);
+    if (want != q.policy()) q.set_policy(want, q.kappa_num(), q.kappa_den());
+  }
   const int policy = q.policy();
+  p.policy = policy;
+  steps_by_policy_[policy] += 1;
   const bool limited = cfg_.kv_capacity > 0;
   // 1. every running request grows by one position this step
   int64_t need = 0;

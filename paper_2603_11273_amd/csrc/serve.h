@@ -39,6 +39,10 @@ struct ServeConfig {
   int32_t cross_tokens = 0;    // positions charged for a request's cross cache
   int32_t tok_num = 27, tok_den = 10;   // output tokens per audio-second (rational)
   int32_t start_token = 0;     // decoder input at position 0
+  // dynamic policy switching (0: the queue's policy throughout)
+  int32_t dynamic = 0;
+  int32_t depth_low = 0;       // eligible waiting <= depth_low: FCFS
+  int64_t starve_num = 0, starve_den = 1;   // some ratio above this: HRRN, else SJF
 };
 
 struct RunEntry {
@@ -52,6 +56,7 @@ struct RunEntry {
 };
 
 struct ServePlan {
+  int32_t policy = 0;                     // policy the step ran under
   std::vector<int64_t> preempted;
   std::vector<int64_t> admitted;          // ids, prefilled this step
   std::vector<int32_t> admitted_slot;
@@ -88,6 +93,13 @@ class ServeEngine {
   bool take_result(int64_t id, std::vector<int32_t>* tokens);
   bool has_result(int64_t id) const;
   const RunEntry* find(int64_t id) const;
+  int64_t steps_under(int policy) const { return steps_by_policy_[policy]; }
+
+  // The dynamic rule: FCFS while at most depth_low requests wait (every one
+  // of them is about to be admitted anyway, so arrival order costs nothing);
+  // otherwise HRRN as soon as some waiting request's response ratio exceeds
+  // the starvation threshold, else SJF.
+  int choose_policy(int64_t now_us, const WaitQueue& q) const;
 
  private:
   // true when running entry a is evicted before b at time now
@@ -97,6 +109,7 @@ class ServeEngine {
   std::vector<RunEntry> run_;                 // admission order
   std::vector<int32_t> free_slots_;
   int64_t seq_ = 0;
+  int64_t steps_by_policy_[3] = {0, 0, 0};
   std::vector<std::pair<int64_t, std::vector<int32_t>>> done_;
 };
 

@@ -125,6 +125,24 @@ def test_percentile_nearest_rank_matches_numpy():
             assert S.percentile_nearest_rank(v, p) == int(np.percentile(v, p, method="inverted_cdf"))
 
 
+def test_oracle_dynamic_rule_by_hand():
+    """The switching rule on hand-built queues at now = 10 s (depth_low 2,
+    starvation threshold ratio 3): two eligible requests -> FCFS whatever
+    their waits; three short waits -> SJF; one request waiting 9 s for a 4 s
+    job (ratio (9 + 4) / 4 = 3.25 > 3) -> HRRN; a request not yet arrived
+    counts for nothing."""
+    R = lambda rid, arr_s, dur_s: Q.Req(rid, int(arr_s * 1e6), 0, SR, int(dur_s * 1e6), 448)  # noqa: E731
+    now = 10_000_000
+    three = Fraction(3)
+    assert S.dynamic_policy([R(1, 0, 1), R(2, 1, 9)], now, 2, three) == Q.FCFS
+    assert S.dynamic_policy([R(1, 0, 1), R(2, 1, 9), R(3, 12, 1)], now, 2, three) == Q.FCFS
+    assert S.dynamic_policy([R(1, 9, 1), R(2, 9.5, 2), R(3, 8, 5)], now, 2, three) == Q.SJF
+    # ratios: (1 + 1)/1 = 2, (0.5 + 2)/2 = 1.25, (2 + 5)/5 = 1.4 -> no starvation
+    assert S.dynamic_policy([R(1, 9, 1), R(2, 9.5, 2), R(3, 1, 4)], now, 2, three) == Q.HRRN
+    # the boundary is strict: ratio exactly 3 ((8 + 4)/4) stays SJF
+    assert S.dynamic_policy([R(1, 9, 1), R(2, 9.5, 2), R(3, 2, 4)], now, 2, three) == Q.SJF
+
+
 # --------------------------------------------------------------------------- native vs oracle
 def test_native_toy_example():
     g = _toy()
@@ -162,6 +180,49 @@ CASES = [
     (Q.SJF, 32, 8, 12 * 100 + 448, 100, 200, 0.0, True, True),
     (Q.FCFS, 32, 8, 12 * 100 + 448, 100, 200, 0.0, True, True),
 ]
+
+
+DYN = dict(dynamic=True, depth_low=4, starve=(3, 1))
+CASES_DYN = [
+    (Q.FCFS, 16, 4, 0, 1500, 200, 60.0, False, False),
+    (Q.SJF, 16, 4, 8 * 100 + 448, 100, 200, 80.0, True, False),
+    (Q.HRRN, 32, 8, 12 * 100 + 448, 100, 300, 0.0, False, True),
+]
+
+
+def _engines(case, seed, dyn=None):
+    policy, slots, admit, cap, cross, n, rate, uniform, burst = case
+    ns, arr = _workload(seed + n, n, rate, uniform, burst)
+    c = _ctx(policy, n_slots=slots, max_admit=admit, kv_capacity=cap, cross_tokens=cross)
+    kw = {}
+    if dyn:
+        c.serve_config(kv_capacity=cap, cross_tokens=cross, max_admit=admit, **dyn)
+        kw = dict(dynamic=True, depth_low=dyn["depth_low"], starve=Fraction(*dyn["starve"]))
+    eng = S.Engine(policy, n_slots=slots, max_admit=admit, kv_capacity=cap, cross_tokens=cross,
+                   **kw)
+    for i in range(n):
+        c.submit(i, None, n_samples=ns[i], arrival_us=arr[i])
+        eng.submit(i, ns[i], SR, arr[i])
+    return c, eng, n
+
+
+@pytest.mark.parametrize("case", CASES_DYN)
+def test_native_dynamic_steps_match_oracle(case):
+    c, eng, n = _engines(case, 20260350, DYN)
+    t, done, seen = 0, 0, set()
+    while done < n:
+        got = c.serve_plan(t)
+        ref = eng.step(t)
+        assert got["policy"] == ref.policy, t
+        assert got["preempted"] == ref.preempted, t
+        assert list(zip(got["admitted"], got["admitted_slot"])) == ref.admitted, t
+        assert got["decoded"] == ref.decoded, t
+        assert got["finished"] == ref.finished, t
+        done += len(ref.finished)
+        seen.add(ref.policy)
+        t += 40_000
+    assert c.serve_stats() == eng.steps_by_policy
+    assert len(seen) >= 2, "the case was meant to switch policies"
 
 
 @pytest.mark.parametrize("case", CASES)
