@@ -323,28 +323,78 @@ def serving_section(ctx, D, P, enc_ms, dec_ms, toks, steps_done):
     seed = synth.WORKLOADS["large-v3-decode"].seed + 7
     ns = synth.n_samples_of(synth.durations_lognormal(seed, n_burst))
     clips = [synth.pcm_clip(seed, i, int(ns[i])) for i in range(n_burst)]
-    ctx.set_policy(asr.HRRN)
-    ctx.serve_config(kv_capacity=0, cross_tokens=1500, max_admit=P, start_token=50258)
-    for i, pcm in enumerate(clips):
-        ctx.submit(10**7 + i, pcm, arrival_us=0)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    done, n_steps, n_tok, t_virtual = 0, 0, 0, 0
-    while done < n_burst:
-        r = ctx.serve_step(0)
-        n_steps += 1
-        n_tok += len(r["decoded"])
-        t_virtual += (cost["prefill_us"] * len(r["admitted"]) +
-                      (cost["step_us"] + cost["row_us"] * len(r["decoded"]) if r["decoded"] else 0))
-        for rid in r["finished"]:
-            ctx.serve_tokens(rid)
-        done += len(r["finished"])
-    wall = time.perf_counter() - t0
-    gpu = {"requests": n_burst, "policy": "HRRN", "steps": n_steps, "output_tokens": n_tok,
-           "wall_s": round(wall, 3), "req_per_s": round(n_burst / wall, 1),
-           "tok_per_s": round(n_tok / wall, 1),
-           "virtual_clock_s": round(t_virtual * 1e-6, 3)}
+    def burst(overlap, id0):
+        ctx.set_policy(asr.HRRN)
+        ctx.serve_config(kv_capacity=0, cross_tokens=1500, max_admit=P, start_token=50258,
+                         overlap=overlap)
+        for i, pcm in enumerate(clips):
+            ctx.submit(id0 + i, pcm, arrival_us=0)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        done, n_steps, n_tok, t_virtual = 0, 0, 0, 0
+        while done < n_burst:
+            r = ctx.serve_step(0)
+            n_steps += 1
+            n_tok += len(r["decoded"])
+            t_virtual += (cost["prefill_us"] * len(r["admitted"]) +
+                          (cost["step_us"] + cost["row_us"] * len(r["decoded"])
+                           if r["decoded"] else 0))
+            for rid in r["finished"]:
+                ctx.serve_tokens(rid)
+            done += len(r["finished"])
+        wall = time.perf_counter() - t0
+        return {"requests": n_burst, "policy": "HRRN", "steps": n_steps, "output_tokens": n_tok,
+                "wall_s": round(wall, 3), "req_per_s": round(n_burst / wall, 1),
+                "tok_per_s": round(n_tok / wall, 1), "virtual_clock_s": round(t_virtual * 1e-6, 3)}
+
+    gpu = burst(False, 10**7)
     log(f"GPU burst: {gpu}")
+
+    # real-time Poisson serving on the GPU (arrivals on the wall clock), with
+    # and without the prefill overlapped on a second stream: most steps then
+    # admit a few requests while up to 128 others decode
+    def realtime(overlap, id0, rate, seconds):
+        n = int(rate * seconds)
+        s3 = seed + 99
+        n_s = synth.n_samples_of(synth.durations_lognormal(s3, n))
+        arr = synth.poisson_arrivals_us(s3, n, rate)
+        ctx.set_policy(asr.HRRN)
+        ctx.serve_config(kv_capacity=0, cross_tokens=1500, max_admit=P, start_token=50258,
+                         overlap=int(overlap))
+        for i in range(n):
+            ctx.submit(id0 + i, clips[i % n_burst][:int(n_s[i])], arrival_us=int(arr[i]))
+        first, fin, steps, busy = {}, {}, 0, 0.0
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        while len(fin) < n:
+            now = int((time.perf_counter() - t0) * 1e6)
+            ts = time.perf_counter()
+            r = ctx.serve_step(now)
+            te = time.perf_counter()
+            end_us = int((te - t0) * 1e6)
+            if r["decoded"]:
+                steps += 1
+                busy += te - ts
+            for rid in r["decoded"]:
+                first.setdefault(rid, end_us)
+            for rid in r["finished"]:
+                fin[rid] = end_us
+                ctx.serve_tokens(rid)
+            if not r["decoded"] and not r["admitted"]:
+                time.sleep(0.0002)
+        ttft = np.array([first[id0 + i] - arr[i] for i in range(n)]) * 1e-6
+        e2el = np.array([fin[id0 + i] - arr[i] for i in range(n)]) * 1e-6
+        pct = lambda v, p: round(float(np.percentile(v, p, method="inverted_cdf")), 4)  # noqa: E731
+        return {"requests": n, "rate_per_s": rate, "ttft_p50_s": pct(ttft, 50),
+                "ttft_p90_s": pct(ttft, 90), "e2el_p50_s": pct(e2el, 50),
+                "e2el_p90_s": pct(e2el, 90), "busy_steps": steps,
+                "mean_busy_step_ms": round(busy * 1e3 / max(steps, 1), 3)}
+
+    rt_rate = round(0.6 * gpu["req_per_s"], 1)
+    rt = {"sequential": realtime(0, 3 * 10**7, rt_rate, 4.0),
+          "overlapped_prefill": realtime(1, 4 * 10**7, rt_rate, 4.0),
+          "overlapped_prefill_32_cus_reserved": realtime(32, 5 * 10**7, rt_rate, 4.0)}
+    log(f"GPU real-time serving: {rt}")
 
     # 3. the paper's evaluation on the virtual clock
     DYNAMIC = 3
@@ -397,6 +447,7 @@ def serving_section(ctx, D, P, enc_ms, dec_ms, toks, steps_done):
                 k: round(100.0 * (case[pol][k] - base[k]) / base[k], 1) if base[k] else None
                 for k in ("ttft_p50_s", "ttft_p90_s", "e2el_p50_s", "e2el_p90_s")}
     return {"cost_model_us": cost, "decode_16_rows_ms": round(dec16_ms, 3), "gpu_burst": gpu,
+            "gpu_realtime_poisson": rt,
             "simulation": sim,
             "note": "virtual clock with the costs measured above; lognormal durations stand in "
                     "for LibriSpeech test-clean; 128 slots, up to 64 prefills per step; "

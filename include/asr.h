@@ -241,6 +241,15 @@ typedef struct {
   int32_t depth_low;
   int64_t starve_num;
   int64_t starve_den;   /* > 0 when dynamic */
+  /* >= 1: overlapped prefill (Section 4.1 runs the engine with chunked
+   * prefill).  An admitted request then produces its first token in the step
+   * after the one that prefills it, so a step's prefill runs on a second
+   * stream while the running rows decode on the bound stream.  A value above
+   * 1 is the number of CUs the prefill's persistent GEMMs leave free for the
+   * decode rows.  Every request's tokens are the same as without overlap.
+   * On a queue-only context only the schedule changes (first tokens one step
+   * later). */
+  int32_t overlap;
 } asr_serve_cfg;
 
 /* Arrays are the caller's, each with room for cap >= the slot count

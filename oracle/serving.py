@@ -25,7 +25,7 @@ Readings where the paper is silent (the same ones the engine takes):
   could not fit the pool even alone is refused at submission (it could never
   finish);
 * an admitted request is prefilled and produces its first token in the step
-  that admits it;
+  that admits it (or, with overlapped prefill, in the next step);
 * tokens per request: round-half-up(duration * rate), clamped to
   [1, min(448, max_tokens)];
 * a token position that a recomputed request produces again is not emitted
@@ -111,6 +111,7 @@ class Engine:
     dynamic: bool = False
     depth_low: int = 0
     starve: Fraction = Fraction(0)
+    defer_first: bool = False     # admitted requests start decoding in the next step
     queue: Q.Queue = None
     known: dict = field(default_factory=dict)
     running: list = field(default_factory=list)
@@ -165,9 +166,11 @@ class Engine:
             admitted.append((req.rid, slot))
         for req in requeue:
             self.queue.reqs[req.rid] = req
-        decoded = [r.req.rid for r in self.running]
+        new_ids = {rid for rid, _ in admitted} if self.defer_first else set()
+        rows = [r for r in self.running if r.req.rid not in new_ids]
+        decoded = [r.req.rid for r in rows]
         generated, finished = {}, []
-        for r in list(self.running):
+        for r in rows:
             r.generated += 1
             generated[r.req.rid] = r.generated
             if r.generated >= r.total:

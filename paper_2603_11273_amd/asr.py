@@ -55,7 +55,7 @@ class ServeCfg(C.Structure):
     _fields_ = [("kv_capacity", C.c_int64), ("cross_tokens", C.c_int32),
                 ("max_admit", C.c_int32), ("tok_num", C.c_int32), ("tok_den", C.c_int32),
                 ("start_token", C.c_int32), ("dynamic", C.c_int32), ("depth_low", C.c_int32),
-                ("starve_num", C.c_int64), ("starve_den", C.c_int64)]
+                ("starve_num", C.c_int64), ("starve_den", C.c_int64), ("overlap", C.c_int32)]
 
 
 class ServeOut(C.Structure):
@@ -283,10 +283,12 @@ class Context:
 
     # -- continuous batching ----------------------------------------------------
     def serve_config(self, kv_capacity=0, cross_tokens=1500, max_admit=1, tok_num=27,
-                     tok_den=10, start_token=0, dynamic=False, depth_low=0, starve=(0, 1)):
-        """starve = (num, den): the response-ratio threshold of the dynamic rule."""
+                     tok_den=10, start_token=0, dynamic=False, depth_low=0, starve=(0, 1),
+                     overlap=False):
+        """starve = (num, den): the response-ratio threshold of the dynamic rule;
+        overlap: prefill on a second stream beside the running rows' decode."""
         cfg = ServeCfg(kv_capacity, cross_tokens, max_admit, tok_num, tok_den, start_token,
-                       int(dynamic), depth_low, starve[0], starve[1])
+                       int(dynamic), depth_low, starve[0], starve[1], int(overlap))  # >1: CUs kept free
         _check(lib.asr_serve_config(self.h, C.byref(cfg)))
         self._serve_cap = max(self.cfg.max_slots, 1)
 

@@ -69,6 +69,9 @@ void gemm_bf16(const AView& a, const bf16_t* w, int M, int N, int K, const Epilo
 void gemm_f32(const AView& a, const float* w, int M, int N, int K, const Epilogue& e,
               hipStream_t s);
 
+// Number of CUs the persistent bf16 GEMM leaves free (process-wide; 0 = none).
+void gemm_set_cu_reserve(int n);
+
 // Skinny GEMM for decode rows: partial[s][b][n] = sum_{k in split s} x[b][k] w[n][k].
 // Returns the number of K-splits used (the partial buffer holds splits*D*N floats).
 int dgemm_bf16(const bf16_t* x, const bf16_t* w, int D, int N, int K, float* partial,

@@ -960,6 +960,11 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16_ps(AView a,
 #undef PS_READ
 }
 
+// CUs the persistent GEMM leaves free (0 by default); set while a prefill
+// runs beside decode work on another stream, so that work finds CUs.
+static int g_ps_reserve = 0;
+void gemm_set_cu_reserve(int n) { g_ps_reserve = n < 0 ? 0 : n; }
+
 template <int BM, int BN, int BK, int WM, int WN, int S, int KIND>
 static void launch_gemm_ps(const AView& a, const bf16_t* w, int M, int N, int K,
                            const Epilogue& e, hipStream_t s, int gm) {
@@ -978,7 +983,9 @@ static void launch_gemm_ps(const AView& a, const bf16_t* w, int M, int N, int K,
     attr = true;
   }
   const int n_tm = (M + BM - 1) / BM, n_tn = (N + BN - 1) / BN;
-  const int grid = std::min(n_tm * n_tn, n_cu);
+  // keep the grid a multiple of 8 (one share per XCD) when CUs are reserved
+  const int avail = g_ps_reserve > 0 ? std::max(8, (n_cu - g_ps_reserve) / 8 * 8) : n_cu;
+  const int grid = std::min(n_tm * n_tn, avail);
   kfn<<<grid, WM * WN * 64, lds, s>>>(a, w, M, N, K, e, n_tm, n_tn, gm);
 }
 

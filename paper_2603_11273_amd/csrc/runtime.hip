@@ -112,6 +112,10 @@ struct asr_ctx {
   // continuous batching (asr_serve_*): the engine owns the slots while on
   ServeEngine serve;
   bool serve_mode = false;
+  bool serve_overlap = false;       // prefill on a second stream beside the decode rows
+  int overlap_reserve = 0;          // CUs its persistent GEMMs leave to the decode rows
+  hipStream_t pstream = nullptr;    // that stream (non-blocking, default priority)
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   std::unordered_map<int64_t, Request> serving;   // admitted, not finished (audio kept
                                                   // for a re-prefill after preemption)
   Layout L;
@@ -843,6 +847,10 @@ asr_status asr_destroy(asr_ctx* c) {
   if (c->device >= 0) {
     (void)hipSetDevice(c->device);
     for (auto e : c->ev_pool) (void)hipEventDestroy(e);
+    if (c->pstream) (void)hipStreamSynchronize(c->pstream);
+    if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
+    if (c->ev_join) (void)hipEventDestroy(c->ev_join);
+    if (c->pstream) (void)hipStreamDestroy(c->pstream);
   }
   delete c;
   return ASR_OK;
@@ -1020,14 +1028,26 @@ asr_status asr_slot_info(const asr_ctx* c, int32_t slot, int32_t* occupied, int6
 
 namespace {
 
-// Prefill: audio of reqs[i] -> mel -> stem -> encoder -> cross K/V of slot slots[i].
-asr_status run_prefill(asr_ctx* c, const std::vector<const Request*>& reqs,
-                       const std::vector<int32_t>& slots) {
+// Host arrays a prefill's copies read; they must outlive the stream's sync.
+struct PrefillStage {
+  std::vector<const float*> ptrs;
+  std::vector<int64_t> ns;
+  std::vector<int32_t> slots;
+};
+
+// Prefill: audio of reqs[i] -> mel -> stem -> encoder -> cross K/V of slot
+// slots[i], enqueued on c->stream (no synchronisation).
+asr_status launch_prefill(asr_ctx* c, const std::vector<const Request*>& reqs,
+                          const std::vector<int32_t>& slots_in, PrefillStage& stage) {
   const int P = (int)reqs.size();
   if (P == 0) return ASR_OK;
   hipStream_t s = c->stream;
-  std::vector<const float*> ptrs(P);
-  std::vector<int64_t> ns(P);
+  std::vector<const float*>& ptrs = stage.ptrs;
+  std::vector<int64_t>& ns = stage.ns;
+  std::vector<int32_t>& slots = stage.slots;
+  ptrs.assign(P, nullptr);
+  ns.assign(P, 0);
+  slots = slots_in;
   bool any_host = false;
   for (int i = 0; i < P; ++i) {
     ns[i] = reqs[i]->n_samples;
@@ -1052,11 +1072,18 @@ asr_status run_prefill(asr_ctx* c, const std::vector<const Request*>& reqs,
     if (st != ASR_OK) return st;
   }
   pm.end();
-  // the pageable host vectors and the small pointer arrays above must outlive
-  // the copies that read them
-  HIPCHK(hipStreamSynchronize(s));
   (void)any_host;
   return ASR_OK;
+}
+
+asr_status run_prefill(asr_ctx* c, const std::vector<const Request*>& reqs,
+                       const std::vector<int32_t>& slots) {
+  PrefillStage stage;
+  asr_status st = launch_prefill(c, reqs, slots, stage);
+  // the host arrays of the stage (and the pageable clips) must outlive the
+  // copies that read them
+  HIPCHK(hipStreamSynchronize(c->stream));
+  return st;
 }
 
 // Decode rows (slot, token, position) -> argmax (and logits when asked).
@@ -1193,6 +1220,9 @@ asr_status asr_serve_config(asr_ctx* c, const asr_serve_cfg* sc) {
   }
   if (sc->dynamic && (sc->depth_low < 0 || sc->starve_num < 0 || sc->starve_den <= 0))
     return fail(ASR_EINVAL, "dynamic policy: depth_low >= 0, starve_num >= 0, starve_den > 0");
+  c->serve_overlap = sc->overlap != 0;
+  c->overlap_reserve = sc->overlap > 1 ? sc->overlap : 0;
+  cfg.defer_first = sc->overlap != 0;
   cfg.dynamic = sc->dynamic != 0;
   cfg.depth_low = sc->depth_low;
   cfg.starve_num = sc->starve_num;
@@ -1297,12 +1327,37 @@ asr_status asr_serve_step(asr_ctx* c, int64_t now_us, asr_serve_out* out) {
     if (!r.has_audio) return fail(ASR_EINVAL, "request " + std::to_string(id) + " has no samples");
     reqs.push_back(&r);
   }
-  st = run_prefill(c, reqs, p.admitted_slot);
-  if (st != ASR_OK) return st;
-  const int D = (int)p.dec_id.size();
+  const int D = (int)p.dec_id.size(), A = (int)p.admitted.size();
   std::vector<int32_t> tok(D);
-  st = run_decode(c, D, p.dec_slot.data(), p.dec_token.data(), p.dec_pos, tok.data(), nullptr);
-  if (st != ASR_OK) return st;
+  if (c->serve_overlap && A > 0 && D > 0) {
+    // With overlap the engine defers an admitted request's first token to
+    // the next step, so this step's decode rows do not depend on its prefill:
+    // the prefill runs on a second stream while the rows decode on the bound
+    // stream.  The two share only read-only weights and disjoint slots.
+    if (!c->pstream) {
+      HIPCHK(hipStreamCreateWithFlags(&c->pstream, hipStreamNonBlocking));
+      HIPCHK(hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming));
+      HIPCHK(hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming));
+    }
+    hipStream_t main_stream = c->stream;
+    HIPCHK(hipEventRecord(c->ev_fork, main_stream));
+    HIPCHK(hipStreamWaitEvent(c->pstream, c->ev_fork, 0));
+    PrefillStage stage;
+    c->stream = c->pstream;
+    gemm_set_cu_reserve(c->overlap_reserve);
+    st = launch_prefill(c, reqs, p.admitted_slot, stage);
+    gemm_set_cu_reserve(0);
+    c->stream = main_stream;
+    if (st == ASR_OK)
+      st = run_decode(c, D, p.dec_slot.data(), p.dec_token.data(), p.dec_pos, tok.data(), nullptr);
+    HIPCHK(hipStreamSynchronize(c->pstream));    // the prefill and its stage's host arrays
+    if (st != ASR_OK) return st;
+  } else {
+    st = run_prefill(c, reqs, p.admitted_slot);
+    if (st != ASR_OK) return st;
+    st = run_decode(c, D, p.dec_slot.data(), p.dec_token.data(), p.dec_pos, tok.data(), nullptr);
+    if (st != ASR_OK) return st;
+  }
   serve_finish(c, p, tok.data(), out);
   return collect_timing(c);
 }

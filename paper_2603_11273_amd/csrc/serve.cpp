@@ -99,8 +99,11 @@ ServePlan ServeEngine::plan(int64_t now_us, WaitQueue& q) {
     run_.push_back(std::move(r));
   }
   for (auto& e : requeue) q.push(e);
-  // 3. decode rows: everything running, in admission order
-  for (const auto& r : run_) {
+  // 3. decode rows: everything running, in admission order (with defer_first
+  //    the requests admitted in this step wait for the next one)
+  const size_t n_rows = cfg_.defer_first ? run_.size() - p.admitted.size() : run_.size();
+  for (size_t i = 0; i < n_rows; ++i) {
+    const RunEntry& r = run_[i];
     p.dec_id.push_back(r.q.id);
     p.dec_slot.push_back(r.slot);
     p.dec_pos.push_back(r.generated);

@@ -14,8 +14,9 @@
 //      in it), stopping at the first request the pool cannot hold, at the
 //      per-step admission limit, or when no slot is free;
 //   3. the decode rows are the surviving running requests (admission order)
-//      followed by the admitted ones; after the step each has one more token
-//      and leaves when it reaches its token count.
+//      followed by the admitted ones (not those, with defer_first: they then
+//      start decoding in the next step); after the step each row has one more
+//      token and a request leaves when it reaches its token count.
 //
 // KV pool accounting (in token positions): a running request holds
 // cross_tokens (its cross-attention cache) plus one position per generated
@@ -43,6 +44,9 @@ struct ServeConfig {
   int32_t dynamic = 0;
   int32_t depth_low = 0;       // eligible waiting <= depth_low: FCFS
   int64_t starve_num = 0, starve_den = 1;   // some ratio above this: HRRN, else SJF
+  // admitted requests produce their first token in the step after the one
+  // that prefills them (so a step's prefill and its decode rows are independent)
+  int32_t defer_first = 0;
 };
 
 struct RunEntry {

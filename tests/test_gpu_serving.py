@@ -92,20 +92,22 @@ def test_serve_greedy_matches_oracle_under_preemption():
 
 def test_serve_batch_invariance():
     """Whisper-base shape with 2+2 layers, bf16: the same 8 requests served
-    with 8 slots and no pool limit, with 3 slots, and with 8 slots under
-    pressure (HRRN) give every request bit-identical tokens."""
+    with 8 slots and no pool limit, with 3 slots, with 8 slots under pressure
+    (HRRN), and with the prefill overlapped on a second stream, give every
+    request bit-identical tokens."""
     from paper_2603_11273_amd import asr
     shape = synth.reduced_shape(synth.SHAPES["base"], 2, 2)
     seed = 20260341
     clips, arr = _requests(seed, 8)
     runs = []
-    for slots, cap, cross, pol in ((8, 0, 1500, asr.FCFS), (3, 0, 1500, asr.SJF),
-                                   (8, 40, 10, asr.HRRN)):
+    for slots, cap, cross, pol, ov in ((8, 0, 1500, asr.FCFS, False), (3, 0, 1500, asr.SJF, False),
+                                       (8, 40, 10, asr.HRRN, False), (4, 0, 1500, asr.SJF, True)):
         ctx = make_context(shape, seed, max_slots=slots, max_prefill=2, max_decode=slots)
-        toks, pre = _serve(ctx, pol, clips, arr, kv_capacity=cap, cross_tokens=cross, max_admit=2)
+        toks, pre = _serve(ctx, pol, clips, arr, kv_capacity=cap, cross_tokens=cross, max_admit=2,
+                           overlap=ov)
         runs.append((toks, pre))
         del ctx
         torch.cuda.empty_cache()
     assert runs[2][1] > 0
     for i in range(len(clips)):
-        assert runs[0][0][i] == runs[1][0][i] == runs[2][0][i], f"request {i}"
+        assert runs[0][0][i] == runs[1][0][i] == runs[2][0][i] == runs[3][0][i], f"request {i}"

@@ -206,6 +206,32 @@ def _engines(case, seed, dyn=None):
     return c, eng, n
 
 
+@pytest.mark.parametrize("case", CASES[3:6])
+def test_native_deferred_first_token_matches_oracle(case):
+    """Overlapped-prefill schedule: admitted requests decode from the next
+    step on (pool pressure cases)."""
+    policy, slots, admit, cap, cross, n, rate, uniform, burst = case
+    ns, arr = _workload(20260360 + n, n, rate, uniform, burst)
+    c = _ctx(policy, n_slots=slots, max_admit=admit, kv_capacity=cap, cross_tokens=cross)
+    c.serve_config(kv_capacity=cap, cross_tokens=cross, max_admit=admit, overlap=True)
+    eng = S.Engine(policy, n_slots=slots, max_admit=admit, kv_capacity=cap, cross_tokens=cross,
+                   defer_first=True)
+    for i in range(n):
+        c.submit(i, None, n_samples=ns[i], arrival_us=arr[i])
+        eng.submit(i, ns[i], SR, arr[i])
+    t, done = 0, 0
+    while done < n:
+        got = c.serve_plan(t)
+        ref = eng.step(t)
+        assert got["preempted"] == ref.preempted, t
+        assert list(zip(got["admitted"], got["admitted_slot"])) == ref.admitted, t
+        assert got["decoded"] == ref.decoded, t
+        assert not set(got["decoded"]) & set(got["admitted"])
+        assert got["finished"] == ref.finished, t
+        done += len(ref.finished)
+        t += 40_000
+
+
 @pytest.mark.parametrize("case", CASES_DYN)
 def test_native_dynamic_steps_match_oracle(case):
     c, eng, n = _engines(case, 20260350, DYN)
