@@ -1299,32 +1299,49 @@ template void dgemm_reduce<bf16_t>(const float*, int, int, int, const float*, in
                                    hipStream_t);
 
 // Split-K reduce fused with the residual add and the next LayerNorm: one
-// block per decode row; the row (d <= 2048) stays in registers, 4 values per
-// thread:  h[b] += bias + sum_s partial[s][b];  xn[b] = LN(h[b]) (eps 1e-5).
+// block per decode row.  Thread t sums the float4 column group t % G (G =
+// d/4) over the splits s = t / G, t / G + SG, ... (SG split groups, unrolled
+// so that several loads are in flight), the SG partial sums meet in LDS, and
+// the G owners finish the row:  h[b] += bias + sum_s partial[s][b];
+// xn[b] = LN(h[b]) (eps 1e-5).
 template <typename T>
-__global__ __launch_bounds__(512) void k_reduce_resid_ln(const float* __restrict__ partial,
-                                                         int splits, int D, int d,
-                                                         const float* __restrict__ bias,
-                                                         float* __restrict__ h,
-                                                         const float* __restrict__ g,
-                                                         const float* __restrict__ beta, T* xn) {
-  __shared__ float red[2][8];
+__global__ __launch_bounds__(1024) void k_reduce_resid_ln(const float* __restrict__ partial,
+                                                          int splits, int D, int d,
+                                                          const float* __restrict__ bias,
+                                                          float* __restrict__ h,
+                                                          const float* __restrict__ g,
+                                                          const float* __restrict__ beta, T* xn) {
+  __shared__ float4 part[1024];
+  __shared__ float red[2][16];
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int nw = blockDim.x >> 6;
-  float v[4];
-  float sum = 0.f;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int n = tid + i * blockDim.x;
-    v[i] = 0.f;
-    if (n < d) {
-      float a = h[(int64_t)b * d + n] + bias[n];
-      for (int s = 0; s < splits; ++s) a += partial[((int64_t)s * D + b) * d + n];
-      h[(int64_t)b * d + n] = a;
-      v[i] = a;
-      sum += a;
+  const int G = d >> 2, SG = blockDim.x / G;
+  const int grp = tid % G, sg = tid / G;
+  const int64_t rs = (int64_t)D * d;                 // stride between splits
+  const float* src = partial + (int64_t)b * d + grp * 4;
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (sg < SG) {
+    int s = sg;
+    for (; s + 3 * SG < splits; s += 4 * SG) {
+      const float4 v0 = *(const float4*)(src + s * rs);
+      const float4 v1 = *(const float4*)(src + (s + SG) * rs);
+      const float4 v2 = *(const float4*)(src + (s + 2 * SG) * rs);
+      const float4 v3 = *(const float4*)(src + (s + 3 * SG) * rs);
+      a = add4(a, add4(add4(v0, v1), add4(v2, v3)));
     }
+    for (; s < splits; s += SG) a = add4(a, *(const float4*)(src + s * rs));
   }
+  part[tid] = a;
+  __syncthreads();
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  float sum = 0.f;
+  if (tid < G) {
+    for (int k = 1; k < SG; ++k) a = add4(a, part[tid + k * G]);
+    float* hp = h + (int64_t)b * d + tid * 4;
+    v = add4(add4(*(const float4*)hp, *(const float4*)(bias + tid * 4)), a);
+    *(float4*)hp = v;
+    sum = (v.x + v.y) + (v.z + v.w);
+  }
+  const int nw = (blockDim.x + 63) >> 6;
   sum = wave_sum(sum);
   if (lane == 0) red[0][wave] = sum;
   __syncthreads();
@@ -1332,10 +1349,9 @@ __global__ __launch_bounds__(512) void k_reduce_resid_ln(const float* __restrict
   for (int w2 = 0; w2 < nw; ++w2) tot += red[0][w2];
   const float mean = tot / d;
   float q = 0.f;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int n = tid + i * blockDim.x;
-    if (n < d) q += (v[i] - mean) * (v[i] - mean);
+  if (tid < G) {
+    const float4 c = make_float4(v.x - mean, v.y - mean, v.z - mean, v.w - mean);
+    q = (c.x * c.x + c.y * c.y) + (c.z * c.z + c.w * c.w);
   }
   q = wave_sum(q);
   if (lane == 0) red[1][wave] = q;
@@ -1343,10 +1359,12 @@ __global__ __launch_bounds__(512) void k_reduce_resid_ln(const float* __restrict
   float var = 0.f;
   for (int w2 = 0; w2 < nw; ++w2) var += red[1][w2];
   const float rstd = rsqrtf(var / d + 1e-5f);
+  if (tid < G) {
+    const float4 gg = *(const float4*)(g + tid * 4), bb = *(const float4*)(beta + tid * 4);
+    const float o[4] = {(v.x - mean) * rstd * gg.x + bb.x, (v.y - mean) * rstd * gg.y + bb.y,
+                        (v.z - mean) * rstd * gg.z + bb.z, (v.w - mean) * rstd * gg.w + bb.w};
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int n = tid + i * blockDim.x;
-    if (n < d) St<T>::st(xn, (int64_t)b * d + n, (v[i] - mean) * rstd * g[n] + beta[n]);
+    for (int k = 0; k < 4; ++k) St<T>::st(xn, (int64_t)b * d + tid * 4 + k, o[k]);
   }
 }
 
@@ -1354,7 +1372,9 @@ template <typename T>
 void reduce_resid_ln(const float* partial, int splits, int D, int d, const float* bias, float* h,
                      const float* g, const float* beta, T* xn, hipStream_t s) {
   if (D <= 0) return;
-  int threads = ((d + 3) / 4 + 63) / 64 * 64;      // 4 values per thread, whole waves
+  const int G = d / 4;                                // d % 64 == 0, d <= 2048
+  const int SG = std::max(1, 1024 / G);
+  const int threads = (G * SG + 63) / 64 * 64;
   k_reduce_resid_ln<T><<<D, threads, 0, s>>>(partial, splits, D, d, bias, h, g, beta, xn);
 }
 template void reduce_resid_ln<float>(const float*, int, int, int, const float*, float*,
