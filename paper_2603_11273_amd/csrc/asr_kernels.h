@@ -116,13 +116,20 @@ void flash_attn_f32(const float* qkv, float* out, int B, int n_head, hipStream_t
 
 // Decode attention.  Self: writes k, v of each row at its slot position, then
 // attends over position + 1 keys.  Cross: attends over 1500 cached keys.
+// Keys are split into chunks handled by separate blocks; `part` (at least
+// decode_attn_part_floats(D, n_head) floats) holds the per-chunk partials
+// that a combine kernel merges into out.
+constexpr int DA_NCH = 4;    // chunks per row at most (1500 cross keys / 384)
+constexpr int DA_REC = 66;   // floats per partial: max, sum, 64 weighted values
+int decode_attn_part_floats(int D, int n_head);
 template <typename T>
 void decode_self_attn(const T* qkv, T* cache, int64_t slot_stride, int64_t layer_off,
                       const int32_t* slots, const int32_t* pos, int D, int n_head, T* out,
-                      hipStream_t s);
+                      float* part, hipStream_t s);
 template <typename T>
 void decode_cross_attn(const T* q, T* cache, int64_t slot_stride, int64_t layer_off,
-                       const int32_t* slots, int D, int n_head, T* out, hipStream_t s);
+                       const int32_t* slots, int D, int n_head, T* out, float* part,
+                       hipStream_t s);
 
 template <typename T>
 void embed(const T* tok_emb, const float* pos_emb, const int32_t* tokens, const int32_t* pos,

@@ -311,28 +311,39 @@ __device__ __forceinline__ void load8(const bf16_t* p, float* v) {
 
 // Block of 256 threads; lane group of 8 lanes per key (8 dims each), 4 waves
 // x 8 keys = 32 keys per pass, 4 passes unrolled per loop iteration.
+// Keys per block of the decode attention: a row's keys are split into chunks
+// of DA_CK handled by separate blocks (flash-decoding), which fills the chip
+// in whole rounds (128 rows x 20 heads x 4 chunks of the 1500 cross keys =
+// 10240 blocks = 5 rounds of 2048 resident blocks); a combine kernel merges
+// the chunks' (max, sum, weighted values).
+constexpr int DA_CK = 384;
+
 template <typename T, bool SELF>
 __global__ __launch_bounds__(256) void k_decode_attn(const T* __restrict__ src, T* cache,
                                                      int64_t slot_stride, int64_t layer_off,
                                                      const int32_t* slots, const int32_t* pos,
-                                                     int n_head, T* __restrict__ out) {
+                                                     int n_head, float* __restrict__ part) {
   constexpr int CTX = SELF ? kTextCtx : kCtx;
   __shared__ float qs[64];
-  __shared__ float sc[CTX];
+  __shared__ float sc[DA_CK];
   __shared__ float red[4];
   __shared__ float ored[4][64];
-  const int h = blockIdx.x, row = blockIdx.y;
+  const int h = blockIdx.x, row = blockIdx.y, chunk = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int d = n_head * 64;
   const int ldsrc = SELF ? 3 * d : d;
-  const int slot = slots[row];
   const int n = SELF ? pos[row] + 1 : kCtx;
+  const int k0 = chunk * DA_CK;
+  if (k0 >= n) return;                          // this row has fewer chunks (uniform per block)
+  const int kn = min(DA_CK, n - k0);            // keys of this chunk
+  const int slot = slots[row];
   T* kb = cache + (int64_t)slot * slot_stride + layer_off + (int64_t)h * CTX * 64;
   T* vb = kb + (int64_t)n_head * CTX * 64;
   const T* srow = src + (int64_t)row * ldsrc + h * 64;
 
   if (tid < 64) qs[tid] = St<T>::ld(srow, tid) * 0.125f;
-  if (SELF && tid < 128) {                      // store this step's k, v at position n-1
+  if (SELF && tid < 128 && n - 1 >= k0 && n - 1 < k0 + kn) {
+    // the chunk holding position n-1 stores this step's k, v there
     int j = tid & 63;
     if (tid < 64)
       kb[(int64_t)(n - 1) * 64 + j] = srow[d + j];
@@ -346,42 +357,42 @@ __global__ __launch_bounds__(256) void k_decode_attn(const T* __restrict__ src, 
 #pragma unroll
   for (int i = 0; i < 8; ++i) qv[i] = qs[dc + i];
 
-  // scores
-  for (int g0 = 0; g0 < n; g0 += 128) {
-    float part[4];
+  // scores of the chunk's keys (8 lanes per key, 16-byte loads)
+  for (int g0 = 0; g0 < kn; g0 += 128) {
+    float partial[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      int key = g0 + u * 32 + wave * 8 + sub;
-      part[u] = 0.f;
-      if (key < n) {
+      const int kk = g0 + u * 32 + wave * 8 + sub, key = k0 + kk;
+      partial[u] = 0.f;
+      if (kk < kn) {
         const T* kp = (SELF && key == n - 1) ? (srow + d) : (kb + (int64_t)key * 64);
         float kv[8];
         load8(kp + dc, kv);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) part[u] = fmaf(qv[i], kv[i], part[u]);
+        for (int i = 0; i < 8; ++i) partial[u] = fmaf(qv[i], kv[i], partial[u]);
       }
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      float p = part[u];
+      float p = partial[u];
       p += __shfl_xor(p, 1, 64);
       p += __shfl_xor(p, 2, 64);
       p += __shfl_xor(p, 4, 64);
-      int key = g0 + u * 32 + wave * 8 + sub;
-      if ((lane & 7) == 0 && key < n) sc[key] = p;
+      const int kk = g0 + u * 32 + wave * 8 + sub;
+      if ((lane & 7) == 0 && kk < kn) sc[kk] = p;
     }
   }
   __syncthreads();
 
   float mx = -INFINITY;
-  for (int k = tid; k < n; k += 256) mx = fmaxf(mx, sc[k]);
+  for (int k = tid; k < kn; k += 256) mx = fmaxf(mx, sc[k]);
   mx = wave_max(mx);
   if (lane == 0) red[wave] = mx;
   __syncthreads();
   mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   __syncthreads();
   float sum = 0.f;
-  for (int k = tid; k < n; k += 256) {
+  for (int k = tid; k < kn; k += 256) {
     float p = expf(sc[k] - mx);
     sc[k] = p;
     sum += p;
@@ -389,21 +400,21 @@ __global__ __launch_bounds__(256) void k_decode_attn(const T* __restrict__ src, 
   sum = wave_sum(sum);
   if (lane == 0) red[wave] = sum;
   __syncthreads();
-  const float inv = 1.0f / (red[0] + red[1] + red[2] + red[3]);
+  const float l = red[0] + red[1] + red[2] + red[3];
 
-  // probability-weighted values
+  // probability-weighted values of the chunk
   float acc[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = 0.f;
-  for (int g0 = 0; g0 < n; g0 += 128) {
+  for (int g0 = 0; g0 < kn; g0 += 128) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      int key = g0 + u * 32 + wave * 8 + sub;
-      if (key < n) {
+      const int kk = g0 + u * 32 + wave * 8 + sub, key = k0 + kk;
+      if (kk < kn) {
         const T* vp = (SELF && key == n - 1) ? (srow + 2 * d) : (vb + (int64_t)key * 64);
         float vv[8];
         load8(vp + dc, vv);
-        float p = sc[key];
+        const float p = sc[kk];
 #pragma unroll
         for (int i = 0; i < 8; ++i) acc[i] = fmaf(p, vv[i], acc[i]);
       }
@@ -422,34 +433,67 @@ __global__ __launch_bounds__(256) void k_decode_attn(const T* __restrict__ src, 
     for (int i = 0; i < 8; ++i) ored[wave][dc + i] = acc[i];
   }
   __syncthreads();
-  if (tid < 64) {
-    float v = ored[0][tid] + ored[1][tid] + ored[2][tid] + ored[3][tid];
-    St<T>::st(out, (int64_t)row * d + h * 64 + tid, v * inv);
+  // partial record of (row, head, chunk): [max, sum, 64 weighted values]
+  float* rec = part + (((int64_t)row * n_head + h) * DA_NCH + chunk) * DA_REC;
+  if (tid < 64) rec[2 + tid] = ored[0][tid] + ored[1][tid] + ored[2][tid] + ored[3][tid];
+  if (tid == 0) {
+    rec[0] = mx;
+    rec[1] = l;
   }
 }
+
+// out[row][h] = sum_c e^{m_c - M} acc_c / sum_c e^{m_c - M} l_c over the
+// row's chunks (M = max_c m_c).  One wave per (row, head).
+template <typename T, bool SELF>
+__global__ __launch_bounds__(256) void k_decode_combine(const float* __restrict__ part,
+                                                        const int32_t* pos, int D, int n_head,
+                                                        T* __restrict__ out) {
+  const int w = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (w >= D * n_head) return;
+  const int row = w / n_head, h = w - row * n_head;
+  const int n = SELF ? pos[row] + 1 : kCtx;
+  const int nch = (n + DA_CK - 1) / DA_CK;
+  const float* rec = part + (int64_t)w * DA_NCH * DA_REC;
+  float M = -INFINITY;
+  for (int c = 0; c < nch; ++c) M = fmaxf(M, rec[c * DA_REC]);
+  float num = 0.f, den = 0.f;
+  for (int c = 0; c < nch; ++c) {
+    const float f = expf(rec[c * DA_REC] - M);
+    den += f * rec[c * DA_REC + 1];
+    num += f * rec[c * DA_REC + 2 + lane];
+  }
+  St<T>::st(out, (int64_t)row * n_head * 64 + h * 64 + lane, num / den);
+}
+
+int decode_attn_part_floats(int D, int n_head) { return D * n_head * DA_NCH * DA_REC; }
 
 template <typename T>
 void decode_self_attn(const T* qkv, T* cache, int64_t slot_stride, int64_t layer_off,
                       const int32_t* slots, const int32_t* pos, int D, int n_head, T* out,
-                      hipStream_t s) {
-  if (D > 0)
-    k_decode_attn<T, true><<<dim3(n_head, D), 256, 0, s>>>(qkv, cache, slot_stride, layer_off,
-                                                           slots, pos, n_head, out);
+                      float* part, hipStream_t s) {
+  if (D <= 0) return;
+  constexpr int nch = (kTextCtx + DA_CK - 1) / DA_CK;
+  k_decode_attn<T, true><<<dim3(n_head, D, nch), 256, 0, s>>>(qkv, cache, slot_stride, layer_off,
+                                                              slots, pos, n_head, part);
+  k_decode_combine<T, true><<<(D * n_head + 3) / 4, 256, 0, s>>>(part, pos, D, n_head, out);
 }
 template <typename T>
 void decode_cross_attn(const T* q, T* cache, int64_t slot_stride, int64_t layer_off,
-                       const int32_t* slots, int D, int n_head, T* out, hipStream_t s) {
-  if (D > 0)
-    k_decode_attn<T, false><<<dim3(n_head, D), 256, 0, s>>>(q, cache, slot_stride, layer_off,
-                                                            slots, nullptr, n_head, out);
+                       const int32_t* slots, int D, int n_head, T* out, float* part,
+                       hipStream_t s) {
+  if (D <= 0) return;
+  constexpr int nch = (kCtx + DA_CK - 1) / DA_CK;
+  k_decode_attn<T, false><<<dim3(n_head, D, nch), 256, 0, s>>>(q, cache, slot_stride, layer_off,
+                                                               slots, nullptr, n_head, part);
+  k_decode_combine<T, false><<<(D * n_head + 3) / 4, 256, 0, s>>>(part, nullptr, D, n_head, out);
 }
 template void decode_self_attn<float>(const float*, float*, int64_t, int64_t, const int32_t*,
-                                      const int32_t*, int, int, float*, hipStream_t);
+                                      const int32_t*, int, int, float*, float*, hipStream_t);
 template void decode_self_attn<bf16_t>(const bf16_t*, bf16_t*, int64_t, int64_t, const int32_t*,
-                                       const int32_t*, int, int, bf16_t*, hipStream_t);
+                                       const int32_t*, int, int, bf16_t*, float*, hipStream_t);
 template void decode_cross_attn<float>(const float*, float*, int64_t, int64_t, const int32_t*,
-                                       int, int, float*, hipStream_t);
+                                       int, int, float*, float*, hipStream_t);
 template void decode_cross_attn<bf16_t>(const bf16_t*, bf16_t*, int64_t, int64_t,
-                                        const int32_t*, int, int, bf16_t*, hipStream_t);
+                                        const int32_t*, int, int, bf16_t*, float*, hipStream_t);
 
 }  // namespace asr

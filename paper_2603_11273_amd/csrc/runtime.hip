@@ -85,7 +85,8 @@ struct Layout {
          h1 = 0, x = 0, xn = 0, qkv = 0, vt = 0, att = 0, hid = 0, p_slots = 0;
   size_t vt_bytes = 0;
   size_t d_slots = 0, d_tokens = 0, d_pos = 0, d_h = 0, d_xn = 0, d_qkv = 0, d_q = 0, d_att = 0,
-         d_hid = 0, d_partial = 0, d_logits = 0, d_keys = 0, d_argmax = 0, d_flag = 0;
+         d_hid = 0, d_partial = 0, d_apart = 0, d_logits = 0, d_keys = 0, d_argmax = 0,
+         d_flag = 0;
   size_t wstage = 0;
   int64_t wstage_floats = 0;
   int max_splits = 1;
@@ -310,6 +311,7 @@ void plan(asr_ctx* c) {
     if (c->cfg.dtype != ASR_BF16) most = Nmax;
     L.d_partial = b.take(std::max<int64_t>(most, Nmax) * D * f4);
   }
+  L.d_apart = b.take((int64_t)decode_attn_part_floats((int)D, g.n_head) * f4);
   L.d_logits = b.take(D * (int64_t)std::max(1, g.vocab) * f4);
   L.d_keys = b.take(D * (int64_t)vocab_tiles(std::max(1, g.vocab)) * 8);
   L.d_argmax = b.take(D * 4);
@@ -733,7 +735,7 @@ asr_status decode_rows(asr_ctx* c, int D, const std::vector<int32_t>& pos_host, 
     const int64_t self_off = (int64_t)l * 2 * H * kTextCtx * kHeadDim;
     timed(c, ASR_K_DATTN, 4.0 * self_keys * 64 * H, self_keys * 2 * 64 * H * c->es, [&] {
       decode_self_attn<T>(qkv, self_cache, L.self_stride, self_off, slots, pos, D, H, att,
-                          c->stream);
+                          c->at<float>(L.d_apart), c->stream);
     });
     dgemm_resid_ln<T>(c, att, w.o_w, D, d, w.o_b, h, w.lnx_g, w.lnx_b, xn);
     dgemm_any<T>(c, xn, w.xq_w, D, d, d, w.xq_b, 0, q);
@@ -741,7 +743,7 @@ asr_status decode_rows(asr_ctx* c, int D, const std::vector<int32_t>& pos_host, 
     timed(c, ASR_K_DATTN, 4.0 * D * H * (double)kCtx * 64, (double)D * H * kCtx * 2 * 64 * c->es,
           [&] {
             decode_cross_attn<T>(q, cross_cache, L.cross_stride, cross_off, slots, D, H, att,
-                                 c->stream);
+                                 c->at<float>(L.d_apart), c->stream);
           });
     dgemm_resid_ln<T>(c, att, w.xo_w, D, d, w.xo_b, h, w.ln2_g, w.ln2_b, xn);
     dgemm_any<T>(c, xn, w.fc1_w, D, F, d, w.fc1_b, 1, hid);
