@@ -42,9 +42,13 @@ enum EpiKind : int32_t {
   EPI_CONV1 = 3,      // h1[g][t+1][n] = gelu(acc + bias[n]); h1[g][0][n] = 0 (storage)
   EPI_CONV2 = 4,      // x[r][n] = gelu(acc + bias[n]) + pos[r % 1500][n]   (float32)
   EPI_XKV = 5,        // cross cache of slot[g], all decoder layers        (storage)
-  EPI_QKV = 6,        // q, k -> out[r][n] (n < 2d); v -> out2 = V^T per head (storage)
+  EPI_QKV = 6,        // q (x kQScaleLog2), k -> out[r][n] (n < 2d); v -> out2 = V^T (storage)
   EPI_F32 = 7,        // out[r][n] = acc + bias[n]                       (float32)
 };
+
+// EPI_QKV stores q multiplied by 1/sqrt(64) * log2(e): the encoder's flash
+// attention then works in the exp2 domain without a per-score multiply.
+constexpr float kQScaleLog2 = 0.125f * 1.4426950408889634f;
 
 // Row stride (positions) of the per-head transposed V written by EPI_QKV:
 // V^T[b][h][dim][kVtLd], positions 1500..1535 stay zero.

@@ -43,7 +43,7 @@ constexpr int FA_KT = 64;          // keys per tile
 __device__ __forceinline__ int fa_swz(int row) { return (row >> 1) & 7; }
 
 template <int NW>
-__global__ __launch_bounds__(NW * 64) void k_flash_bf16(const bf16_t* __restrict__ qkv,
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) void k_flash_bf16(const bf16_t* __restrict__ qkv,
                                                        const bf16_t* __restrict__ vt,
                                                        bf16_t* __restrict__ out, int n_head) {
   constexpr int NTH = NW * 64;
@@ -100,8 +100,12 @@ __global__ __launch_bounds__(NW * 64) void k_flash_bf16(const bf16_t* __restrict
   f32x16 o0, o1;                                   // O^T dims 0..31, 32..63
 #pragma unroll
   for (int r = 0; r < 16; ++r) o0[r] = o1[r] = 0.f;
-  float m = -INFINITY, l = 0.f;
-  const float sc = 0.125f * 1.4426950408889634f;  // 1/sqrt(64) * log2(e)
+  // Q arrives pre-scaled by 1/sqrt(64) * log2(e) (the QKV product's epilogue
+  // folds the factor in before its one bf16 rounding), so scores are in the
+  // exp2 domain.  The S accumulators start at -m, the lane's query reference,
+  // so the MFMAs deliver s - m directly; the first tile sets m to its own
+  // maximum (m = 0 before it).
+  float m = 0.f, l = 0.f;
   const int sw = fa_swz(l32);
   const int vhalf = (half ^ ((l32 >> 4) & 1)) * 4;
 
@@ -117,10 +121,11 @@ __global__ __launch_bounds__(NW * 64) void k_flash_bf16(const bf16_t* __restrict
     const bf16_t* Vc = Vs[cur];
 
     f32x16 s[2];
+    const float s_init = -m;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
+      for (int r = 0; r < 16; ++r) s[kb][r] = s_init;
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
         const bf16x8 kf =
@@ -143,23 +148,32 @@ __global__ __launch_bounds__(NW * 64) void k_flash_bf16(const bf16_t* __restrict
 #pragma unroll
       for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, s[kb][r]);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    // Lazy rescaling: the running reference m only moves (and O, l are only
+    // Lazy rescaling: the reference m only moves (and O, l are only
     // rescaled) when some query of the wave sees a score more than 2^8 above
-    // it in the exp2 domain.  Until then the probabilities exp2((s - m) sc)
-    // may exceed 1 by up to 256x, which fp32 sums and bf16 operands carry
-    // with unchanged relative precision; the final 1/l cancels the offset.
-    if (__any((tmax - m) * sc > 8.0f)) {
-      const float mnew = fmaxf(m, tmax);
-      const float alpha = __builtin_amdgcn_exp2f((m - mnew) * sc);   // 0 on the first tile
-      m = mnew;
+    // it.  Until then the probabilities exp2(s - m) may exceed 1 by up to
+    // 256x, which fp32 sums and bf16 operands carry with unchanged relative
+    // precision; the final 1/l cancels the offset.
+    if (kt == 0) {
+      m = tmax;                                    // 64 real keys: finite
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[kb][r] -= tmax;
+    } else if (__any(tmax > 8.0f)) {
+      const float shift = fmaxf(tmax, 0.f);
+      const float alpha = __builtin_amdgcn_exp2f(-shift);
+      m += shift;
       l *= alpha;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         o0[r] *= alpha;
         o1[r] *= alpha;
       }
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[kb][r] -= shift;
     }
-    const float nb = -m * sc;
     float psum = 0.f;
     bf16x8 pb[2][2];                               // [kb][hf]
 #pragma unroll
@@ -171,7 +185,7 @@ __global__ __launch_bounds__(NW * 64) void k_flash_bf16(const bf16_t* __restrict
         for (int i = 0; i < 8; ++i) {
           // exp2 of a value <= 8; results below 2^-126 flush to 0, far below
           // the bf16 resolution of a probability next to the row's maximum
-          p[i] = __builtin_amdgcn_exp2f(fmaf(s[kb][hf * 8 + i], sc, nb));
+          p[i] = __builtin_amdgcn_exp2f(s[kb][hf * 8 + i]);
           psum += p[i];
         }
         uint4 u = {pack2_bf16(p[0], p[1]), pack2_bf16(p[2], p[3]), pack2_bf16(p[4], p[5]),

@@ -54,7 +54,7 @@ __device__ __forceinline__ void epi_apply(const Epilogue& e, int r, int n, float
   } else if constexpr (KIND == EPI_QKV) {
     const int two_d = 2 * e.d_model;
     if (n < two_d) {
-      St<T>::st((T*)e.out, (int64_t)r * e.ldc + n, v);
+      St<T>::st((T*)e.out, (int64_t)r * e.ldc + n, n < e.d_model ? v * kQScaleLog2 : v);
     } else {
       int g = r / kCtx, t = r - g * kCtx;
       int hd = n - two_d;
@@ -92,7 +92,11 @@ __device__ __forceinline__ float4 add4(float4 a, float4 b) {
 template <int KIND>
 __device__ __forceinline__ void epi_apply4(const Epilogue& e, int r, int n, float4 v) {
   if (e.bias) v = add4(v, *(const float4*)(e.bias + n));
-  if constexpr (KIND == EPI_STORE || KIND == EPI_QKV) {
+  if constexpr (KIND == EPI_QKV) {
+    if (n < e.d_model) v = make_float4(v.x * kQScaleLog2, v.y * kQScaleLog2, v.z * kQScaleLog2,
+                                       v.w * kQScaleLog2);
+    st4_bf16((bf16_t*)e.out + (int64_t)r * e.ldc + n, v);
+  } else if constexpr (KIND == EPI_STORE) {
     st4_bf16((bf16_t*)e.out + (int64_t)r * e.ldc + n, v);
   } else if constexpr (KIND == EPI_GELU) {
     st4_bf16((bf16_t*)e.out + (int64_t)r * e.ldc + n, gelu4(v));
