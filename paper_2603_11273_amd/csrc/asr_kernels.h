@@ -38,12 +38,10 @@ struct AView {
 enum EpiKind : int32_t {
   EPI_STORE = 0,      // out[r][n] = acc + bias[n]                       (storage type)
   EPI_GELU = 1,       // out[r][n] = gelu(acc + bias[n])                 (storage type)
-  EPI_RESID = 2,      // x[r][n] += acc + bias[n]                        (float32)
   EPI_CONV1 = 3,      // h1[g][t+1][n] = gelu(acc + bias[n]); h1[g][0][n] = 0 (storage)
   EPI_CONV2 = 4,      // x[r][n] = gelu(acc + bias[n]) + pos[r % 1500][n]   (float32)
   EPI_XKV = 5,        // cross cache of slot[g], all decoder layers        (storage)
   EPI_QKV = 6,        // q (x kQScaleLog2), k -> out[r][n] (n < 2d); v -> out2 = V^T (storage)
-  EPI_F32 = 7,        // out[r][n] = acc + bias[n]                       (float32)
 };
 
 // EPI_QKV stores q multiplied by 1/sqrt(64) * log2(e): the encoder's flash
@@ -57,7 +55,7 @@ constexpr int kVtLd = 1536;
 struct Epilogue {
   int32_t kind;
   void* out;            // destination (type depends on kind)
-  int64_t ldc;          // row stride of out (elements) for STORE/GELU/RESID/CONV2
+  int64_t ldc;          // row stride of out (elements) for STORE/GELU/CONV2/QKV
   const float* bias;    // [N]
   const float* pos;     // CONV2: sinusoid table [1500][N]
   const int32_t* slots; // XKV: slot of each clip
@@ -108,9 +106,10 @@ int vocab_tiles(int V);
 template <typename T>
 void layer_norm(const float* x, int rows, int d, const float* g, const float* b, T* out,
                 hipStream_t s);
-// Residual add fused with the LayerNorm that follows it: x += y, out = LN(x).
+// Residual add fused with the LayerNorm that follows it: x += y, out = LN(x)
+// (the residual branch y in storage type T, the stream x in float32).
 template <typename T>
-void residual_layer_norm(float* x, const float* y, int rows, int d, const float* g,
+void residual_layer_norm(float* x, const T* y, int rows, int d, const float* g,
                          const float* b, T* out, hipStream_t s);
 
 // Encoder self-attention over 1500 positions, qkv [B*1500][3d], out [B*1500][d].

@@ -27,9 +27,6 @@ __device__ __forceinline__ void epi_apply(const Epilogue& e, int r, int n, float
     St<T>::st((T*)e.out, (int64_t)r * e.ldc + n, v);
   } else if constexpr (KIND == EPI_GELU) {
     St<T>::st((T*)e.out, (int64_t)r * e.ldc + n, gelu_erf(v));
-  } else if constexpr (KIND == EPI_RESID) {
-    float* x = (float*)e.out + (int64_t)r * e.ldc + n;
-    *x = *x + v;
   } else if constexpr (KIND == EPI_CONV1) {
     int g = r / kFrames, t = r - g * kFrames;
     int64_t base = (int64_t)g * (kFrames + 1) * e.d_model;
@@ -49,8 +46,6 @@ __device__ __forceinline__ void epi_apply(const Epilogue& e, int r, int n, float
     int64_t addr = (int64_t)e.slots[g] * e.slot_stride +
                    ((((int64_t)l * 2 + kv) * e.n_head + h) * kCtx + t) * kHeadDim + c;
     St<T>::st((T*)e.out, addr, v);
-  } else if constexpr (KIND == EPI_F32) {
-    ((float*)e.out)[(int64_t)r * e.ldc + n] = v;
   } else if constexpr (KIND == EPI_QKV) {
     const int two_d = 2 * e.d_model;
     if (n < two_d) {
@@ -88,10 +83,9 @@ __device__ __forceinline__ float4 add4(float4 a, float4 b) {
   return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
 }
 
-// Four consecutive columns n..n+3 of row r (n % 4 == 0), bias not yet added.
+// Four consecutive columns n..n+3 of row r (n % 4 == 0), bias already added.
 template <int KIND>
 __device__ __forceinline__ void epi_apply4(const Epilogue& e, int r, int n, float4 v) {
-  if (e.bias) v = add4(v, *(const float4*)(e.bias + n));
   if constexpr (KIND == EPI_QKV) {
     if (n < e.d_model) v = make_float4(v.x * kQScaleLog2, v.y * kQScaleLog2, v.z * kQScaleLog2,
                                        v.w * kQScaleLog2);
@@ -100,11 +94,6 @@ __device__ __forceinline__ void epi_apply4(const Epilogue& e, int r, int n, floa
     st4_bf16((bf16_t*)e.out + (int64_t)r * e.ldc + n, v);
   } else if constexpr (KIND == EPI_GELU) {
     st4_bf16((bf16_t*)e.out + (int64_t)r * e.ldc + n, gelu4(v));
-  } else if constexpr (KIND == EPI_F32) {
-    st4_f32((float*)e.out + (int64_t)r * e.ldc + n, v);
-  } else if constexpr (KIND == EPI_RESID) {
-    float* x = (float*)e.out + (int64_t)r * e.ldc + n;
-    st4_f32(x, add4(*(const float4*)x, v));
   } else if constexpr (KIND == EPI_CONV1) {
     const int g = r / kFrames, t = r - g * kFrames;
     const int64_t base = (int64_t)g * (kFrames + 1) * e.d_model;
@@ -124,6 +113,19 @@ __device__ __forceinline__ void epi_apply4(const Epilogue& e, int r, int n, floa
                          (hd & 63);
     st4_bf16((bf16_t*)e.out + addr, v);
   }
+}
+
+// Bias of the four columns n..n+3 (zero without bias or past N).  The
+// epilogues load it once per wave tile, ahead of the block loop: a load per
+// block would put an L2 round trip on the epilogue's critical path 2 FM FN
+// times.
+__device__ __forceinline__ float4 bias4(const Epilogue& e, int n, int N) {
+  if (!e.bias || n >= N) return make_float4(0.f, 0.f, 0.f, 0.f);
+  if (n + 3 < N) return *(const float4*)(e.bias + n);
+  return make_float4(e.bias[n], n + 1 < N ? e.bias[n + 1] : 0.f, n + 2 < N ? e.bias[n + 2] : 0.f, 0.f);
+}
+__device__ __forceinline__ float bias1(const Epilogue& e, int n, int N) {
+  return e.bias && n < N ? e.bias[n] : 0.f;
 }
 
 // Epilogue of a wave's FM x FN accumulator blocks.  Each 32x32 block goes
@@ -149,6 +151,18 @@ __device__ __forceinline__ void epi_wave_impl(const Epilogue& e, f32x16 (&acc)[F
   const int l32 = lane & 31, lh = lane >> 5;
   const bool vec_ok = (N & 3) == 0 && (e.ldc & 3) == 0 && (e.d_model & 3) == 0;
   constexpr int AK = KIND == EPI_VT ? EPI_QKV : KIND;     // kind for the scalar fallback
+  constexpr int NB = KIND == EPI_VT ? 4 : 1;
+  float4 bj[FN];                // bias of the lane's columns (x only for VT: one per it)
+  float bvt[FN][NB];
+#pragma unroll
+  for (int j = 0; j < FN; ++j) {
+    if constexpr (KIND == EPI_VT) {
+#pragma unroll
+      for (int it = 0; it < NB; ++it) bvt[j][it] = bias1(e, n0w + j * 32 + it * 8 + (lane >> 3), N);
+    } else {
+      bj[j] = bias4(e, n0w + j * 32 + (lane & 7) * 4, N);
+    }
+  }
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -169,7 +183,7 @@ __device__ __forceinline__ void epi_wave_impl(const Epilogue& e, f32x16 (&acc)[F
           float4 v = make_float4(stage[r4 * kStageLd + c], stage[(r4 + 1) * kStageLd + c],
                                  stage[(r4 + 2) * kStageLd + c], stage[(r4 + 3) * kStageLd + c]);
           if (row + 3 < M) {
-            const float b = e.bias ? e.bias[n] : 0.f;
+            const float b = bvt[j][it];
             v = add4(v, make_float4(b, b, b, b));
             const int g = row / kCtx, t = row - g * kCtx;    // t % 4 == 0: same clip
             const int hd = n - 2 * e.d_model;
@@ -190,7 +204,7 @@ __device__ __forceinline__ void epi_wave_impl(const Epilogue& e, f32x16 (&acc)[F
           if (row >= M || n >= N) continue;
           const float4 v = *(const float4*)&stage[rr * kStageLd + c4];
           if (vec_ok) {
-            epi_apply4<KIND>(e, row, n, v);
+            epi_apply4<KIND>(e, row, n, add4(v, bj[j]));
           } else {
             const float vv[4] = {v.x, v.y, v.z, v.w};
             for (int q = 0; q < 4; ++q)
@@ -455,6 +469,12 @@ __device__ __forceinline__ void wait_vmcnt_rt(int n) {
 __device__ __forceinline__ void lds_dma16(uint32_t lds_addr, const void* gptr) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
                :: "s"(lds_addr), "v"(gptr) : "memory", "m0");
+}
+// Same with a wave-uniform 64-bit base in SGPRs and a 32-bit per-lane byte
+// offset: no per-load address arithmetic in vector registers.
+__device__ __forceinline__ void lds_dma16_s(uint32_t lds_addr, uint32_t voff, const void* sbase) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :: "s"(lds_addr), "v"(voff), "s"(sbase) : "memory", "m0");
 }
 
 template <int BM, int BN, int BK, int WM, int WN, int S, int KIND, int SCHED = 0>
@@ -753,6 +773,12 @@ __device__ __forceinline__ void epi_wave_half(const Epilogue& e, f32x16 (&acc)[F
   const int l32 = lane & 31, lh = lane >> 5;
   const bool vec_ok = (N & 3) == 0 && (e.ldc & 3) == 0 && (e.d_model & 3) == 0;
   const bool vt = KIND == EPI_QKV && n0w >= 2 * e.d_model;   // wave-uniform
+  float4 bj[FN];     // bias of the lane's columns: c4..c4+3, or (VT) columns it*16 + lane/4
+#pragma unroll
+  for (int j = 0; j < FN; ++j)
+    bj[j] = vt ? make_float4(bias1(e, n0w + j * 32 + (lane >> 2), N),
+                             bias1(e, n0w + j * 32 + 16 + (lane >> 2), N), 0.f, 0.f)
+               : bias4(e, n0w + j * 32 + (lane & 7) * 4, N);
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -774,7 +800,7 @@ __device__ __forceinline__ void epi_wave_half(const Epilogue& e, f32x16 (&acc)[F
             float4 v = make_float4(stage[r4 * kStageLd + c], stage[(r4 + 1) * kStageLd + c],
                                    stage[(r4 + 2) * kStageLd + c], stage[(r4 + 3) * kStageLd + c]);
             if (row + 3 < M) {
-              const float b = e.bias ? e.bias[n] : 0.f;
+              const float b = it == 0 ? bj[j].x : bj[j].y;
               v = add4(v, make_float4(b, b, b, b));
               const int g = row / kCtx, t = row - g * kCtx;    // t % 4 == 0: same clip
               const int hd = n - 2 * e.d_model;
@@ -795,7 +821,7 @@ __device__ __forceinline__ void epi_wave_half(const Epilogue& e, f32x16 (&acc)[F
             if (row >= M || n >= N) continue;
             const float4 v = *(const float4*)&stage[rr * kStageLd + c4];
             if (vec_ok) {
-              epi_apply4<KIND>(e, row, n, v);
+              epi_apply4<KIND>(e, row, n, add4(v, bj[j]));
             } else {
               const float vv[4] = {v.x, v.y, v.z, v.w};
               for (int q = 0; q < 4; ++q)
@@ -809,8 +835,108 @@ __device__ __forceinline__ void epi_wave_half(const Epilogue& e, f32x16 (&acc)[F
 
 #undef EPI_HALF_UNROLL
 
-template <int BM, int BN, int BK, int WM, int WN, int S, int KIND>
-__global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16_ps(AView a,
+// Epilogue straight from registers, for a product formed transposed
+// (W fragment as the MFMA's first operand): a lane then holds output row
+// l32 of each 32x32 block and, in register quad q, the four consecutive
+// columns 8q + 4 lh .. 8q + 4 lh + 3.  The values are packed to bf16 and one
+// lane-half swap (v_permlane32_swap) gathers eight consecutive columns per
+// lane, so each store moves 16 bytes.  Row-major outputs are stored
+// through a buffer resource sized to the output: lanes past M or N get an
+// offset beyond it, which the hardware drops, so no lane diverges.  The
+// cross-attention cache (XKV, far above the 2^31-byte reach of a buffer
+// offset) is addressed per lane: the row part (slot, position) once per
+// tile, the column part (layer, K/V, head, dim) per 16-byte run, which an
+// eight-column run never splits since heads are 64 wide.  No LDS round trip:
+// the store stream issues as fast as the accumulators convert.
+template <int KIND>
+constexpr bool kDirectEpi = KIND == EPI_STORE || KIND == EPI_GELU || KIND == EPI_XKV;
+
+template <int KIND, int FM, int FN>
+__device__ __forceinline__ void epi_direct(const Epilogue& e, f32x16 (&acc)[FM][FN], int m0w,
+                                           int n0w, int M, int N, int lane) {
+  static_assert(kDirectEpi<KIND>, "direct epilogue kind");
+  typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+  const int l32 = lane & 31, lh = lane >> 5;
+  __amdgpu_buffer_rsrc_t rs;
+  int64_t xrow[FM];    // XKV: slot and position part of each of the lane's rows
+  if constexpr (KIND == EPI_XKV) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int r = min(m0w + i * 32 + l32, M - 1), g = r / kCtx;
+      xrow[i] = (int64_t)e.slots[g] * e.slot_stride + (int64_t)(r - g * kCtx) * kHeadDim;
+    }
+  } else {
+    rs = __builtin_amdgcn_make_buffer_rsrc(e.out, (short)0, (int)((int64_t)M * e.ldc * 2),
+                                           0x00020000);
+  }
+  float4 bq[FN][4];
+#pragma unroll
+  for (int j = 0; j < FN; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) bq[j][q] = bias4(e, n0w + j * 32 + 8 * q + 4 * lh, N);
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int row = m0w + i * 32 + l32;
+    const bool rok = row < M;
+    const int rofs = row * (int)e.ldc;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      float v[16];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        v[4 * q] = acc[i][j][4 * q] + bq[j][q].x;
+        v[4 * q + 1] = acc[i][j][4 * q + 1] + bq[j][q].y;
+        v[4 * q + 2] = acc[i][j][4 * q + 2] + bq[j][q].z;
+        v[4 * q + 3] = acc[i][j][4 * q + 3] + bq[j][q].w;
+      }
+      if constexpr (KIND == EPI_GELU) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) v[r] = gelu_erf(v[r]);
+      }
+      {
+        uint32_t o[8];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          o[2 * q] = pack2_bf16(v[4 * q], v[4 * q + 1]);
+          o[2 * q + 1] = pack2_bf16(v[4 * q + 2], v[4 * q + 3]);
+        }
+        // lanes 32-63 of quads 0 / 2 <-> lanes 0-31 of quads 1 / 3: lane l < 32
+        // then holds columns 0-7 (16-23), lane l + 32 columns 8-15 (24-31)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const auto s0 = __builtin_amdgcn_permlane32_swap(o[4 * h], o[4 * h + 2], false, false);
+          const auto s1 = __builtin_amdgcn_permlane32_swap(o[4 * h + 1], o[4 * h + 3], false, false);
+          o[4 * h] = s0[0];
+          o[4 * h + 2] = s0[1];
+          o[4 * h + 1] = s1[0];
+          o[4 * h + 3] = s1[1];
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int n = n0w + j * 32 + 16 * h + 8 * lh;
+          const u32x4 x = {o[4 * h], o[4 * h + 1], o[4 * h + 2], o[4 * h + 3]};
+          if constexpr (KIND == EPI_XKV) {
+            if (rok && n < N) {
+              const int two_d = 2 * e.d_model;
+              const int l = n / two_d, rem = n - l * two_d;
+              const int kv = rem >= e.d_model, hd = rem - kv * e.d_model;
+              const int64_t cofs =
+                  ((((int64_t)l * 2 + kv) * e.n_head + (hd >> 6)) * kCtx) * kHeadDim + (hd & 63);
+              *(u32x4*)((bf16_t*)e.out + xrow[i] + cofs) = x;
+            }
+          } else {
+            const uint32_t off = rok && n < N ? (uint32_t)(rofs + n) * 2u : 0x80000000u;
+            __builtin_amdgcn_raw_buffer_store_b128(x, rs, off, 0, 0);
+          }
+        }
+      }
+    }
+  }
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int S, int KIND, bool SW>
+__global__ __launch_bounds__(WM* WN * 64) __attribute__((amdgpu_waves_per_eu(2)))
+void k_gemm_bf16_ps(AView a,
                                                              const bf16_t* __restrict__ w,
                                                              int M, int N, int K, Epilogue e,
                                                              int n_tm, int n_tn, int gm) {
@@ -841,8 +967,9 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16_ps(AView a,
   const uint32_t lds0 =
       (uint32_t)(uintptr_t)((__attribute__((address_space(3))) bf16_t*)smem);
 
-  // per-wave LDS destinations (fixed) and per-lane source offsets in
-  // elements (32-bit: the launcher checks the operand extents), reset per tile
+  // per-wave LDS destinations (fixed) and per-lane source offsets in bytes
+  // from a wave-uniform base (32-bit: the launcher checks the operand
+  // extents), reset per tile
   uint32_t adst[IA], bdst[IB];
 #pragma unroll
   for (int i = 0; i < IA; ++i)
@@ -863,13 +990,13 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16_ps(AView a,
       const int c = ((lane % CPR) ^ lds_swz<BK>(row)) * 8;
       const int r = min(tm * BM + row, M - 1);
       const int g = r / a.rows_per_batch;
-      aoff[i] = (uint32_t)(g * a.batch_stride + (int64_t)(r - g * a.rows_per_batch) * a.lda + c);
+      aoff[i] = (uint32_t)(g * a.batch_stride + (int64_t)(r - g * a.rows_per_batch) * a.lda + c) * 2u;
     }
 #pragma unroll
     for (int i = 0; i < IB; ++i) {
       const int row = (i * NW + wave) * RPI + lane / CPR;
       const int c = ((lane % CPR) ^ lds_swz<BK>(row)) * 8;
-      boff[i] = (uint32_t)min(tn * BN + row, N - 1) * (uint32_t)K + (uint32_t)c;
+      boff[i] = ((uint32_t)min(tn * BN + row, N - 1) * (uint32_t)K + (uint32_t)c) * 2u;
     }
     src_tile = ti;
   };
@@ -877,11 +1004,12 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16_ps(AView a,
     const int ti = gi / nk, kt = gi - ti * nk;
     if (ti != src_tile) set_src(ti);
     const uint32_t so = (uint32_t)((gi % S) * STAGE * 2);
-    const int k0 = kt * BK;
+    const bf16_t* ak = abase + kt * BK;
+    const bf16_t* bk = w + kt * BK;
 #pragma unroll
-    for (int i = 0; i < IA; ++i) lds_dma16(adst[i] + so, abase + aoff[i] + k0);
+    for (int i = 0; i < IA; ++i) lds_dma16_s(adst[i] + so, aoff[i], ak);
 #pragma unroll
-    for (int i = 0; i < IB; ++i) lds_dma16(bdst[i] + so, w + boff[i] + k0);
+    for (int i = 0; i < IB; ++i) lds_dma16_s(bdst[i] + so, boff[i], bk);
   };
 
   f32x16 acc[FM][FN];
@@ -931,7 +1059,8 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16_ps(AView a,
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[p][i], bfr[p][j], acc[i][j], 0, 0, 0);
+          acc[i][j] = SW ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[p][j], af[p][i], acc[i][j], 0, 0, 0)
+                         : __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[p][i], bfr[p][j], acc[i][j], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
     if (last_k) {
@@ -943,8 +1072,11 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16_ps(AView a,
       }
       int tm, tn;
       tile_of((int)blockIdx.x + ti * grid, n_tiles, n_tm, n_tn, gm, tm, tn);
-      epi_wave_half<KIND, FM, FN>(e, acc, (float*)(smem + S * STAGE) + wave * 16 * kStageLd,
-                                  tm * BM + wm * TM, tn * BN + wn * TN, M, N, lane);
+      if constexpr (SW)
+        epi_direct<KIND, FM, FN>(e, acc, tm * BM + wm * TM, tn * BN + wn * TN, M, N, lane);
+      else
+        epi_wave_half<KIND, FM, FN>(e, acc, (float*)(smem + S * STAGE) + wave * 16 * kStageLd,
+                                    tm * BM + wm * TM, tn * BN + wn * TN, M, N, lane);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -969,12 +1101,12 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16_ps(AView a,
 static int g_ps_reserve = 0;
 void gemm_set_cu_reserve(int n) { g_ps_reserve = n < 0 ? 0 : n; }
 
-template <int BM, int BN, int BK, int WM, int WN, int S, int KIND>
+template <int BM, int BN, int BK, int WM, int WN, int S, int KIND, int OCC = 1, bool SW = false>
 static void launch_gemm_ps(const AView& a, const bf16_t* w, int M, int N, int K,
                            const Epilogue& e, hipStream_t s, int gm) {
   constexpr size_t lds = (size_t)S * (BM + BN) * BK * sizeof(bf16_t) +
-                        (size_t)WM * WN * 16 * kStageLd * sizeof(float);
-  auto kfn = k_gemm_bf16_ps<BM, BN, BK, WM, WN, S, KIND>;
+                        (SW ? 0 : (size_t)WM * WN * 16 * kStageLd * sizeof(float));
+  auto kfn = k_gemm_bf16_ps<BM, BN, BK, WM, WN, S, KIND, SW>;
   static bool attr = false;
   static int n_cu = 0;
   if (!attr) {
@@ -989,16 +1121,24 @@ static void launch_gemm_ps(const AView& a, const bf16_t* w, int M, int N, int K,
   const int n_tm = (M + BM - 1) / BM, n_tn = (N + BN - 1) / BN;
   // keep the grid a multiple of 8 (one share per XCD) when CUs are reserved
   const int avail = g_ps_reserve > 0 ? std::max(8, (n_cu - g_ps_reserve) / 8 * 8) : n_cu;
-  const int grid = std::min(n_tm * n_tn, avail);
+  const int grid = std::min(n_tm * n_tn, OCC * avail);
   kfn<<<grid, WM * WN * 64, lds, s>>>(a, w, M, N, K, e, n_tm, n_tn, gm);
 }
 
-// Operand extents (elements) that the persistent kernel's 32-bit source
-// offsets can address.
+// The register epilogue stores 16-byte runs of eight columns through a
+// buffer resource that spans the output (byte size below 2^31).
+static bool direct_epi_ok(const Epilogue& e, int M, int N) {
+  if (N % 8 != 0 || ((uintptr_t)e.out & 15) != 0) return false;
+  if (e.kind == EPI_XKV) return e.d_model % 64 == 0 && e.slot_stride % 8 == 0;
+  return e.ldc % 8 == 0 && e.ldc >= N && (int64_t)M * e.ldc * 2 < (int64_t)INT32_MAX;
+}
+
+// Operand extents that the persistent kernel's 32-bit byte offsets can
+// address.
 static bool fits_u32_offsets(const AView& a, int M, int N, int K) {
   const int64_t r = M - 1, g = r / a.rows_per_batch;
   const int64_t a_end = g * a.batch_stride + (r - g * a.rows_per_batch) * a.lda + K;
-  return a_end < (int64_t)UINT32_MAX && (int64_t)N * K < (int64_t)UINT32_MAX;
+  return 2 * a_end < (int64_t)UINT32_MAX && 2 * (int64_t)N * K < (int64_t)UINT32_MAX;
 }
 
 template <int BM, int BN, int BK, int WM, int WN, int S, int KIND>
@@ -1075,10 +1215,17 @@ static void launch_gemm_bf16(const AView& a, const bf16_t* w, int M, int N, int 
     // (the scatter epilogues of the stem and of the fused QKV product run
     // slower from the persistent kernel's half-block stage than from the
     // plain kernel's full-block one)
-    if (KIND != EPI_RESID && KIND != EPI_QKV && KIND != EPI_CONV1 &&
-        fits_u32_offsets(a, M, N, K))
-      launch_gemm_ps<256, 256, 64, 2, 4, 2, KIND>(a, w, M, N, K, e, s, N >= 3072 ? 8 : 4);
-    else
+    if (KIND != EPI_QKV && KIND != EPI_CONV1 &&
+        fits_u32_offsets(a, M, N, K)) {
+      const int gm = N >= 3072 ? 8 : 4;
+      if constexpr (kDirectEpi<KIND>) {
+        if (direct_epi_ok(e, M, N)) {
+          launch_gemm_ps<256, 256, 64, 2, 4, 2, KIND, 1, true>(a, w, M, N, K, e, s, gm);
+          return;
+        }
+      }
+      launch_gemm_ps<256, 256, 64, 2, 4, 2, KIND>(a, w, M, N, K, e, s, gm);
+    } else
       launch_gemm_pf<256, 256, 64, 2, 4, 2, KIND>(a, w, M, N, K, e, s, 4);
   } else if (t256x128 >= 512) {
     launch_gemm_pf<256, 128, 32, 4, 2, 3, KIND>(a, w, M, N, K, e, s, 4);
@@ -1093,12 +1240,10 @@ void gemm_bf16(const AView& a, const bf16_t* w, int M, int N, int K, const Epilo
   switch (e.kind) {
     case EPI_STORE: launch_gemm_bf16<EPI_STORE>(a, w, M, N, K, e, s); break;
     case EPI_GELU: launch_gemm_bf16<EPI_GELU>(a, w, M, N, K, e, s); break;
-    case EPI_RESID: launch_gemm_bf16<EPI_RESID>(a, w, M, N, K, e, s); break;
     case EPI_CONV1: launch_gemm_bf16<EPI_CONV1>(a, w, M, N, K, e, s); break;
     case EPI_CONV2: launch_gemm_bf16<EPI_CONV2>(a, w, M, N, K, e, s); break;
     case EPI_XKV: launch_gemm_bf16<EPI_XKV>(a, w, M, N, K, e, s); break;
     case EPI_QKV: launch_gemm_bf16<EPI_QKV>(a, w, M, N, K, e, s); break;
-    case EPI_F32: launch_gemm_bf16<EPI_F32>(a, w, M, N, K, e, s); break;
   }
 }
 
@@ -1163,11 +1308,9 @@ void gemm_f32(const AView& a, const float* w, int M, int N, int K, const Epilogu
   switch (e.kind) {
     case EPI_STORE: launch_gemm_f32<EPI_STORE>(a, w, M, N, K, e, s); break;
     case EPI_GELU: launch_gemm_f32<EPI_GELU>(a, w, M, N, K, e, s); break;
-    case EPI_RESID: launch_gemm_f32<EPI_RESID>(a, w, M, N, K, e, s); break;
     case EPI_CONV1: launch_gemm_f32<EPI_CONV1>(a, w, M, N, K, e, s); break;
     case EPI_CONV2: launch_gemm_f32<EPI_CONV2>(a, w, M, N, K, e, s); break;
     case EPI_XKV: launch_gemm_f32<EPI_XKV>(a, w, M, N, K, e, s); break;
-    case EPI_F32: launch_gemm_f32<EPI_F32>(a, w, M, N, K, e, s); break;
   }
 }
 

@@ -117,8 +117,21 @@ __device__ __forceinline__ void st4<bf16_t>(bf16_t* p, float4 v) {
   *(uint2*)p = u;
 }
 
+template <typename T>
+__device__ __forceinline__ float4 ld4(const T* p);
+template <>
+__device__ __forceinline__ float4 ld4<float>(const float* p) {
+  return *(const float4*)p;
+}
+template <>
+__device__ __forceinline__ float4 ld4<bf16_t>(const bf16_t* p) {
+  const uint2 u = *(const uint2*)p;
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u),
+                     __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u));
+}
+
 template <typename T, int Q, bool RES>
-__global__ __launch_bounds__(256) void k_layer_norm(float* x, const float* y, int rows,
+__global__ __launch_bounds__(256) void k_layer_norm(float* x, const T* y, int rows,
                                                     const float* g, const float* b, T* out) {
   constexpr int d = Q * 256;
   int row = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -132,7 +145,7 @@ __global__ __launch_bounds__(256) void k_layer_norm(float* x, const float* y, in
     const int e = (lane + 64 * i) * 4;
     v[i] = *(const float4*)(xr + e);
     if constexpr (RES) {
-      const float4 t = *(const float4*)(y + (int64_t)row * d + e);
+      const float4 t = ld4<T>(y + (int64_t)row * d + e);
       v[i] = make_float4(v[i].x + t.x, v[i].y + t.y, v[i].z + t.z, v[i].w + t.w);
       *(float4*)(xr + e) = v[i];
     }
@@ -158,7 +171,7 @@ __global__ __launch_bounds__(256) void k_layer_norm(float* x, const float* y, in
 
 // Any d that is a multiple of 64: two passes over global memory.
 template <typename T, bool RES>
-__global__ __launch_bounds__(256) void k_layer_norm_any(float* x, const float* y, int rows,
+__global__ __launch_bounds__(256) void k_layer_norm_any(float* x, const T* y, int rows,
                                                         int d, const float* g, const float* b,
                                                         T* out) {
   int row = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -167,7 +180,7 @@ __global__ __launch_bounds__(256) void k_layer_norm_any(float* x, const float* y
   float* xr = x + (int64_t)row * d;
   float s = 0.f;
   for (int e = lane; e < d; e += 64) {
-    if constexpr (RES) xr[e] += y[(int64_t)row * d + e];
+    if constexpr (RES) xr[e] += St<T>::ld(y, (int64_t)row * d + e);
     s += xr[e];
   }
   float mean = wave_sum(s) / d;
@@ -182,7 +195,7 @@ __global__ __launch_bounds__(256) void k_layer_norm_any(float* x, const float* y
 }
 
 template <typename T, bool RES>
-static void layer_norm_launch(float* x, const float* y, int rows, int d, const float* g,
+static void layer_norm_launch(float* x, const T* y, int rows, int d, const float* g,
                               const float* b, T* out, hipStream_t s) {
   if (rows <= 0) return;
   dim3 grid((rows + 3) / 4);
@@ -202,13 +215,13 @@ void layer_norm(const float* x, int rows, int d, const float* g, const float* b,
 }
 
 template <typename T>
-void residual_layer_norm(float* x, const float* y, int rows, int d, const float* g,
+void residual_layer_norm(float* x, const T* y, int rows, int d, const float* g,
                          const float* b, T* out, hipStream_t s) {
   layer_norm_launch<T, true>(x, y, rows, d, g, b, out, s);
 }
 template void residual_layer_norm<float>(float*, const float*, int, int, const float*,
                                          const float*, float*, hipStream_t);
-template void residual_layer_norm<bf16_t>(float*, const float*, int, int, const float*,
+template void residual_layer_norm<bf16_t>(float*, const bf16_t*, int, int, const float*,
                                           const float*, bf16_t*, hipStream_t);
 template void layer_norm<float>(const float*, int, int, const float*, const float*, float*,
                                 hipStream_t);

@@ -504,11 +504,10 @@ asr_status run_mel(asr_ctx* c, int n) {
 template <typename T>
 void gemm_any(asr_ctx* c, const AView& a, size_t w_off, int M, int N, int K, const Epilogue& e) {
   double flops = 2.0 * M * N * K;
-  // operands read once, result written once; the fp32 residual epilogue also
-  // reads the residual, the second convolution and EPI_F32 write fp32
+  // operands read once, result written once (the second convolution writes
+  // the float32 stream)
   double out_bytes = (double)M * N * c->es;
-  if (e.kind == EPI_RESID) out_bytes = 2.0 * M * N * 4;
-  if (e.kind == EPI_CONV2 || e.kind == EPI_F32) out_bytes = (double)M * N * 4;
+  if (e.kind == EPI_CONV2) out_bytes = (double)M * N * 4;
   double bytes = (double)M * K * c->es + (double)N * K * c->es + out_bytes;
   timed(c, ASR_K_GEMM, flops, bytes, [&] {
     if (c->bf16())
@@ -529,9 +528,9 @@ void ln_any(asr_ctx* c, const float* x, int rows, size_t g, size_t b, T* out) {
 // x += y, then out = LayerNorm(x): the residual add of a block fused with the
 // LayerNorm that follows it.
 template <typename T>
-void res_ln_any(asr_ctx* c, float* x, const float* y, int rows, size_t g, size_t b, T* out) {
+void res_ln_any(asr_ctx* c, float* x, const T* y, int rows, size_t g, size_t b, T* out) {
   const int d = c->cfg.d_model;
-  timed(c, ASR_K_LN, 9.0 * rows * d, (double)rows * d * (12 + c->es), [&] {
+  timed(c, ASR_K_LN, 9.0 * rows * d, (double)rows * d * (8 + 2 * c->es), [&] {
     residual_layer_norm<T>(x, y, rows, d, c->at<float>(g), c->at<float>(b), out, c->stream);
   });
 }
@@ -575,11 +574,11 @@ asr_status encode_clips(asr_ctx* c, int n) {
   T* qkv = c->at<T>(L.qkv);
   T* att = c->at<T>(L.att);
   T* hid = c->at<T>(L.hid);
-  // The residual branches (attention out-projection, FC2) are written in
-  // float32 to y, which borrows the QKV buffer (dead once attention has run,
-  // and at least 4 d bytes per row in either dtype); the LayerNorm kernel that
-  // follows adds y into the stream.
-  float* y = c->at<float>(L.qkv);
+  // The residual branches (attention out-projection, FC2) are written in the
+  // storage type to y, which borrows the QKV buffer (dead once attention has
+  // run); the LayerNorm kernel that follows adds y into the float32 stream,
+  // as a model stored in bf16 adds its bf16 branch outputs to the residual.
+  T* y = c->at<T>(L.qkv);
   if (g.n_enc > 0) ln_any<T>(c, x, R, L.enc[0].ln1_g, L.enc[0].ln1_b, xn);
   for (int l = 0; l < g.n_enc; ++l) {
     const EncLayer& w = L.enc[l];
@@ -609,7 +608,7 @@ asr_status encode_clips(asr_ctx* c, int n) {
     {
       AView a{att, d, 0, R};
       Epilogue e{};
-      e.kind = EPI_F32;
+      e.kind = EPI_STORE;
       e.out = y;
       e.ldc = d;
       e.bias = c->at<float>(w.o_b);
@@ -628,7 +627,7 @@ asr_status encode_clips(asr_ctx* c, int n) {
     {
       AView a{hid, F, 0, R};
       Epilogue e{};
-      e.kind = EPI_F32;
+      e.kind = EPI_STORE;
       e.out = y;
       e.ldc = d;
       e.bias = c->at<float>(w.fc2_b);
