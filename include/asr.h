@@ -328,6 +328,15 @@ asr_status asr_debug_logmel(asr_ctx* ctx, const float* const* pcm, const int64_t
 /* Encoder output (after ln_post) [n][1500][d] float32 of n clips. */
 asr_status asr_debug_encode(asr_ctx* ctx, const float* const* pcm, const int64_t* n_samples,
                             int32_t n, int32_t on_device, float* out);
+/* Encoder self-attention kernel alone on given operands (Section 2's
+ * encoder: softmax(q k^T / sqrt(64)) v per head, heads = consecutive 64-wide
+ * column groups, no mask over the 1500 positions of a clip).  q, k, v, out:
+ * host float32 [n][1500][d], n <= max_prefill.  q is given in the form the
+ * QKV product hands the kernel: the queries times 1/sqrt(64) log2(e), so the
+ * result is out = softmax_2(q k^T) v with softmax_2(s)_j = 2^s_j / sum 2^s.
+ * A bf16 context rounds q, k, v to bf16 on the way in. */
+asr_status asr_debug_attention(asr_ctx* ctx, const float* q, const float* k, const float* v,
+                               int32_t n, float* out);
 /* Fills slots[i] from a given encoder output E [n][1500][d] (float32): the
  * cross K/V of every decoder layer are projected into the slot's cache, the
  * position is reset to 0, the slot holds request id ids[i] (which must have

@@ -28,7 +28,8 @@ EXPORTED = [
     "asr_n_params", "asr_param_numel", "asr_load_weights", "asr_set_policy", "asr_submit",
     "asr_rank", "asr_pop_batch", "asr_queue_len", "asr_step", "asr_release_slot",
     "asr_slot_info", "asr_set_timing", "asr_get_timing", "asr_reset_timing",
-    "asr_debug_logmel", "asr_debug_encode", "asr_debug_set_encoder_out", "asr_debug_get_kv",
+    "asr_debug_logmel", "asr_debug_encode", "asr_debug_attention", "asr_debug_set_encoder_out",
+    "asr_debug_get_kv",
     "asr_debug_set_self_kv", "asr_serve_config", "asr_serve_step", "asr_serve_plan",
     "asr_serve_tokens", "asr_serve_simulate", "asr_serve_stats",
 ]
@@ -114,6 +115,7 @@ def _load():
         "asr_reset_timing": [vp],
         "asr_debug_logmel": [vp, P(vp), P(i64), i32, i32, P(f)],
         "asr_debug_encode": [vp, P(vp), P(i64), i32, i32, P(f)],
+        "asr_debug_attention": [vp, P(f), P(f), P(f), i32, P(f)],
         "asr_debug_set_encoder_out": [vp, P(i32), P(i64), P(i32), i32, vp, i32],
         "asr_debug_get_kv": [vp, i32, i32, P(f)],
         "asr_debug_set_self_kv": [vp, i32, vp, i32, i32],
@@ -414,6 +416,17 @@ class Context:
         _check(lib.asr_debug_encode(self.h, ptrs, ns.ctypes.data_as(C.POINTER(C.c_int64)),
                                     len(clips), int(on_device),
                                     out.ctypes.data_as(C.POINTER(C.c_float))))
+        return out
+
+    def debug_attention(self, q, k, v):
+        """Encoder attention kernel on [n][1500][d] operands; q in the exp2
+        domain (queries times 1/sqrt(64) log2(e))."""
+        q, k, v = (np.ascontiguousarray(x, np.float32) for x in (q, k, v))
+        assert q.shape == k.shape == v.shape and q.shape[1:] == (1500, self.cfg.d_model)
+        out = np.zeros(q.shape, np.float32)
+        fp = C.POINTER(C.c_float)
+        _check(lib.asr_debug_attention(self.h, q.ctypes.data_as(fp), k.ctypes.data_as(fp),
+                                       v.ctypes.data_as(fp), q.shape[0], out.ctypes.data_as(fp)))
         return out
 
     def debug_set_encoder_out(self, slots, ids, steps_left, E, on_device=False):

@@ -112,6 +112,12 @@ template <typename T>
 void residual_layer_norm(float* x, const T* y, int rows, int d, const float* g,
                          const float* b, T* out, hipStream_t s);
 
+// Writes given float32 operands [B*1500][d] where the attention kernels read
+// them (which: 0 = q, scaled by qmul; 1 = k; 2 = v, transposed into vt for
+// bf16, else columns 2d.. of qkv).
+template <typename T>
+void pack_attn_operand(const float* src, int which, int rows, int d, int n_head, float qmul,
+                       T* qkv, T* vt, hipStream_t s);
 // Encoder self-attention over 1500 positions, qkv [B*1500][3d], out [B*1500][d].
 void flash_attn_bf16(const bf16_t* qkv, const bf16_t* vt, bf16_t* out, int B, int n_head,
                      hipStream_t s);

@@ -2,7 +2,7 @@
 //
 //  * flash_attn_bf16: encoder self-attention over the 1500 positions of a
 //    30-s segment (no mask), MFMA-based.  Each wave owns 32 queries; K and
-//    V^T tiles of 64 keys are staged in LDS and shared by the block's 4
+//    V^T tiles of 64 keys are staged in LDS and shared by the block's
 //    waves.  The kernel computes S^T = K Q^T so that, in the MFMA output
 //    layout, each lane holds one query's scores for 16 keys: the row max and
 //    sum need a single cross-lane exchange, the probabilities feed the
@@ -26,7 +26,7 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) {
 // ---------------------------------------------------------------------------
 // Encoder flash attention (bf16)
 //
-// Block = 4 waves x 64 queries of one (clip, head); tiles of 64 keys.  K
+// Block = NW waves x 32 queries of one (clip, head); tiles of 64 keys.  K
 // comes from the fused QKV buffer, V from the per-head transposed copy the
 // QKV GEMM writes (V^T[dim][position], zero past 1500), so both tiles are
 // plain 16-byte row copies into LDS (XOR-swizzled rows, conflict-free).
@@ -34,9 +34,8 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) {
 // layout a lane owns one query and 16 keys, so the row max needs one
 // cross-lane exchange (lane ^ 32), the probabilities (bf16) are directly the
 // B operand of O^T += V^T P^T, and the online-softmax rescale is per lane.
-// The K and V^T fragments read from LDS serve both 32-query groups of a
-// wave.  The 1/sqrt(64) scale and log2(e) fold into one FMA before exp2;
-// only the last key tile needs the position mask.
+// Q arrives scaled by 1/sqrt(64) log2(e), so scores are already in the exp2
+// domain; only the last key tile needs the position mask.
 // ---------------------------------------------------------------------------
 constexpr int FA_KT = 64;          // keys per tile
 
@@ -102,10 +101,12 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
   for (int r = 0; r < 16; ++r) o0[r] = o1[r] = 0.f;
   // Q arrives pre-scaled by 1/sqrt(64) * log2(e) (the QKV product's epilogue
   // folds the factor in before its one bf16 rounding), so scores are in the
-  // exp2 domain.  The S accumulators start at -m, the lane's query reference,
-  // so the MFMAs deliver s - m directly; the first tile sets m to its own
-  // maximum (m = 0 before it).
+  // exp2 domain.
   float m = 0.f, l = 0.f;
+  bool zref = true;                                // every lane of the wave has m == 0
+  f32x16 zero16;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) zero16[r] = 0.f;
   const int sw = fa_swz(l32);
   const int vhalf = (half ^ ((l32 >> 4) & 1)) * 4;
 
@@ -121,17 +122,21 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
     const bf16_t* Vc = Vs[cur];
 
     f32x16 s[2];
-    const float s_init = -m;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[kb][r] = s_init;
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
         const bf16x8 kf =
             *(const bf16x8*)(Kc + (kb * 32 + l32) * 64 + (((kk * 2 + half) ^ sw) * 8));
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[kb], 0, 0, 0);
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], kk == 0 ? zero16 : s[kb], 0,
+                                                        0, 0);
       }
+    }
+    if (!zref) {                                   // wave-uniform: some lane's m moved
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[kb][r] -= m;
     }
     if (k0 + FA_KT > kCtx) {                       // last tile: keys past 1500 do not exist
 #pragma unroll
@@ -148,21 +153,27 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
 #pragma unroll
       for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, s[kb][r]);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    // Lazy rescaling: the reference m only moves (and O, l are only
-    // rescaled) when some query of the wave sees a score more than 2^8 above
-    // it.  Until then the probabilities exp2(s - m) may exceed 1 by up to
-    // 256x, which fp32 sums and bf16 operands carry with unchanged relative
-    // precision; the final 1/l cancels the offset.
+    // Lazy reference: probabilities are exp2(s - m) with m = 0 as long as
+    // every score of the wave stays within 2^6 of it, so the common case
+    // needs no subtraction at all.  exp2(s - m) may then reach 2^64, which
+    // fp32 sums and bf16 operands carry with unchanged relative precision
+    // (both reach 2^127); the final 1/l cancels the offset.  A first tile
+    // whose maximum lies outside [-64, 64] sets m to it; a later score more
+    // than 2^6 above m moves m up and rescales O and l.
     if (kt == 0) {
-      m = tmax;                                    // 64 real keys: finite
+      if (__any(fabsf(tmax) > 64.0f)) {            // 64 real keys: finite
+        m = tmax;
+        zref = false;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) s[kb][r] -= tmax;
-    } else if (__any(tmax > 8.0f)) {
+          for (int r = 0; r < 16; ++r) s[kb][r] -= tmax;
+      }
+    } else if (__any(tmax > 64.0f)) {
       const float shift = fmaxf(tmax, 0.f);
       const float alpha = __builtin_amdgcn_exp2f(-shift);
       m += shift;
+      zref = false;
       l *= alpha;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
@@ -183,7 +194,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
         float p[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          // exp2 of a value <= 8; results below 2^-126 flush to 0, far below
+          // exp2 of a value <= 64; results below 2^-126 flush to 0, far below
           // the bf16 resolution of a probability next to the row's maximum
           p[i] = __builtin_amdgcn_exp2f(s[kb][hf * 8 + i]);
           psum += p[i];
@@ -238,6 +249,41 @@ void flash_attn_bf16(const bf16_t* qkv, const bf16_t* vt, bf16_t* out, int B, in
   dim3 grid((kCtx + NW * 32 - 1) / (NW * 32), n_head, B);
   k_flash_bf16<NW><<<grid, NW * 64, 0, s>>>(qkv, vt, out, n_head);
 }
+
+// Lays given q / k / v ([B*1500][d] float32) out as the encoder attention
+// kernels read them: which = 0, 1 -> columns 0..d-1, d..2d-1 of qkv (q times
+// qmul); which = 2 -> columns 2d..3d-1 (fp32), or V^T [b][h][dim][kVtLd]
+// (bf16).
+template <typename T>
+__global__ void k_pack_attn_operand(const float* __restrict__ src, int which, int rows, int d,
+                                    int n_head, float qmul, T* __restrict__ qkv,
+                                    T* __restrict__ vt) {
+  const int64_t n = (int64_t)rows * d;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = i / d;
+    const int c = (int)(i - r * d);
+    const float x = which == 0 ? src[i] * qmul : src[i];
+    if (which < 2 || vt == nullptr) {
+      St<T>::st(qkv, r * 3 * d + which * d + c, x);
+    } else {
+      const int64_t g = r / kCtx, t = r - g * kCtx;
+      St<T>::st(vt, ((g * n_head + (c >> 6)) * kHeadDim + (c & 63)) * kVtLd + t, x);
+    }
+  }
+}
+template <typename T>
+void pack_attn_operand(const float* src, int which, int rows, int d, int n_head, float qmul,
+                       T* qkv, T* vt, hipStream_t s) {
+  const int64_t n = (int64_t)rows * d;
+  if (n <= 0) return;
+  const int grid = (int)std::min<int64_t>((n + 255) / 256, 65536);
+  k_pack_attn_operand<T><<<grid, 256, 0, s>>>(src, which, rows, d, n_head, qmul, qkv, vt);
+}
+template void pack_attn_operand<float>(const float*, int, int, int, int, float, float*, float*,
+                                       hipStream_t);
+template void pack_attn_operand<bf16_t>(const float*, int, int, int, int, float, bf16_t*,
+                                        bf16_t*, hipStream_t);
 
 // ---------------------------------------------------------------------------
 // Encoder attention, fp32 (one thread per query, 32-key tiles in LDS)

@@ -1530,6 +1530,44 @@ asr_status asr_debug_encode(asr_ctx* c, const float* const* pcm, const int64_t* 
   return collect_timing(c);
 }
 
+asr_status asr_debug_attention(asr_ctx* c, const float* q, const float* k, const float* v,
+                               int32_t n, float* out) {
+  asr_status st = need_gpu(c, true);
+  if (st != ASR_OK) return st;
+  if (!q || !k || !v || !out) return fail(ASR_EINVAL, "NULL argument");
+  if (n <= 0 || n > c->cfg.max_prefill) return fail(ASR_EINVAL, "n out of [1, max_prefill]");
+  if (c->cfg.n_enc == 0) return fail(ASR_EINVAL, "decoder-only context");
+  HIPCHK(hipSetDevice(c->device));
+  const Layout& L = c->L;
+  const int d = c->cfg.d_model, H = c->cfg.n_head, R = n * kCtx;
+  const int64_t cnt = (int64_t)R * d;
+  float* tmp = c->at<float>(L.wstage);
+  const float* src[3] = {q, k, v};
+  for (int which = 0; which < 3; ++which) {
+    HIPCHK(hipMemcpyAsync(tmp, src[which], cnt * 4, hipMemcpyHostToDevice, c->stream));
+    // the bf16 kernel takes q in the exp2 domain as given; the fp32 kernel
+    // applies 1/sqrt(64) itself and uses exp, so it gets q * 8 / log2(e)
+    if (c->bf16())
+      pack_attn_operand<bf16_t>(tmp, which, R, d, H, 1.0f, c->at<bf16_t>(L.qkv),
+                                c->at<bf16_t>(L.vt), c->stream);
+    else
+      pack_attn_operand<float>(tmp, which, R, d, H, 1.0f / kQScaleLog2, c->at<float>(L.qkv),
+                               nullptr, c->stream);
+  }
+  if (c->bf16()) {
+    flash_attn_bf16(c->at<bf16_t>(L.qkv), c->at<bf16_t>(L.vt), c->at<bf16_t>(L.att), n, H,
+                    c->stream);
+    convert_to_f32<bf16_t>(c->at<bf16_t>(L.att), tmp, cnt, c->stream);
+  } else {
+    flash_attn_f32(c->at<float>(L.qkv), c->at<float>(L.att), n, H, c->stream);
+    convert_to_f32<float>(c->at<float>(L.att), tmp, cnt, c->stream);
+  }
+  CHECK_LAUNCH();
+  HIPCHK(hipMemcpyAsync(out, tmp, cnt * 4, hipMemcpyDeviceToHost, c->stream));
+  HIPCHK(hipStreamSynchronize(c->stream));
+  return ASR_OK;
+}
+
 asr_status asr_debug_set_encoder_out(asr_ctx* c, const int32_t* slots, const int64_t* ids,
                                      const int32_t* steps_left, int32_t n, const float* E,
                                      int32_t on_device) {

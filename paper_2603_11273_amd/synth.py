@@ -295,3 +295,35 @@ def token_ids(seed: int, shape, vocab: int) -> np.ndarray:
 def kv_lengths(seed: int, n: int, lo: int = 10, hi: int = 400) -> np.ndarray:
     rng = np.random.default_rng([seed, 23])
     return rng.integers(lo, hi + 1, size=n, dtype=np.int64).astype(np.int32)
+
+
+ATTENTION_CASES = ("small", "first_tile_large", "late_large", "very_negative")
+
+
+def attention_operands(seed: int, n: int, d_model: int, case: str):
+    """q, k, v [n][1500][d] float32 for the encoder attention kernel, every
+    value bf16-exact (sixteenths in [-1/4, 1/4], plus +-1 components).
+
+    Each head's queries and keys are small random parts plus, depending on
+    `case`, a shared +-1 pattern u per head (|u|^2 = 64): 'small' has none;
+    'first_tile_large' adds u to the queries and 1.5 u to keys 0..63;
+    'late_large' adds u to the queries and 1.5 u to keys 900..963;
+    'very_negative' adds u to the queries and -1.5 u to every key.  With q
+    read in the exp2 domain, the structured keys score about +-96 (the rest
+    stay within a few units), which moves the kernel's softmax reference."""
+    assert case in ATTENTION_CASES
+    rng = np.random.default_rng([seed, 29, ATTENTION_CASES.index(case)])
+    shp = (n, N_AUDIO_CTX, d_model)
+    q = rng.integers(-4, 5, size=shp).astype(np.float32) / 16
+    k = rng.integers(-4, 5, size=shp).astype(np.float32) / 16
+    v = rng.integers(-8, 9, size=shp).astype(np.float32) / 8
+    u = rng.choice(np.array([-1.0, 1.0], np.float32), size=(1, 1, d_model))
+    if case != "small":
+        q += u
+        if case == "first_tile_large":
+            k[:, 0:64] += 1.5 * u
+        elif case == "late_large":
+            k[:, 900:964] += 1.5 * u
+        else:
+            k += -1.5 * u
+    return q, k, v
