@@ -1,6 +1,7 @@
 """The seeded generators: the tensor hash equals its scalar definition, and
 generated values are exact in bfloat16."""
 import numpy as np
+import pytest
 import torch
 
 from paper_2603_11273_amd import synth
@@ -42,3 +43,23 @@ def test_workload_distributions():
     assert abs(u.mean() - 15.5) < 0.3
     a = synth.poisson_arrivals_us(1, 5000, 20.0)
     assert np.all(np.diff(a) >= 0) and abs(a[-1] / 1e6 / 5000 - 0.05) < 0.005
+
+
+@pytest.mark.parametrize("case", synth.ATTENTION_CASES)
+def test_attention_operands_exact_and_structured(case):
+    """The attention operands are bf16-exact, and each case puts the scores
+    (exp2 domain, one head) where its docstring says."""
+    q, k, v = synth.attention_operands(5, 1, 128, case)
+    for a in (q, k, v):
+        t = torch.from_numpy(a)
+        assert torch.equal(t.to(torch.bfloat16).to(torch.float32), t)
+    s = q[0][:, :64].astype(np.float64) @ k[0][:, :64].T.astype(np.float64)
+    first, late = s[:, :64].max(axis=1), s[:, 896:960].max(axis=1)
+    if case == "small":
+        assert np.abs(s).max() < 8
+    elif case == "first_tile_large":
+        assert first.min() > 64 and s[:, 64:].max() < 8
+    elif case == "late_large":
+        assert np.abs(first).max() < 8 and late.min() > 64
+    else:
+        assert s.max() < -64
