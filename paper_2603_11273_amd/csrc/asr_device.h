@@ -62,6 +62,26 @@ __device__ __forceinline__ float wave_sum(float v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
   return v;
 }
+// The same sum without LDS round trips: DPP adds within each 16-lane row
+// (quad swaps, half-row and row mirrors), then the gfx950 lane swaps
+// v_permlane16_swap (rows 0<->1, 2<->3) and v_permlane32_swap (halves).
+// Every lane ends with the total.
+#define ASR_DPP_ADD(v, ctrl)                                                               \
+  ((v) + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), (ctrl), 0xF, 0xF, \
+                                                    true)))
+__device__ __forceinline__ float wave_sum_lanes(float v) {
+  v = ASR_DPP_ADD(v, 0xB1);    // quad_perm [1,0,3,2]
+  v = ASR_DPP_ADD(v, 0x4E);    // quad_perm [2,3,0,1]
+  v = ASR_DPP_ADD(v, 0x141);   // row_half_mirror
+  v = ASR_DPP_ADD(v, 0x140);   // row_mirror
+  const uint32_t u = __float_as_uint(v);
+  const auto p16 = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  v = __uint_as_float(p16[0]) + __uint_as_float(p16[1]);
+  const uint32_t w = __float_as_uint(v);
+  const auto p32 = __builtin_amdgcn_permlane32_swap(w, w, false, false);
+  return __uint_as_float(p32[0]) + __uint_as_float(p32[1]);
+}
+#undef ASR_DPP_ADD
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));

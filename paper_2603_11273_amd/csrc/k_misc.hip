@@ -130,42 +130,56 @@ __device__ __forceinline__ float4 ld4<bf16_t>(const bf16_t* p) {
                      __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u));
 }
 
+// All of a row's loads (x, y, gain, bias) are issued before the first
+// store, and the reductions stay in VALU lanes (DPP and lane swaps): the
+// row's two passes over HBM then overlap instead of alternating with waits.
 template <typename T, int Q, bool RES>
-__global__ __launch_bounds__(256) void k_layer_norm(float* x, const T* y, int rows,
-                                                    const float* g, const float* b, T* out) {
+__global__ __launch_bounds__(256) void k_layer_norm(float* __restrict__ x,
+                                                    const T* __restrict__ y, int rows,
+                                                    const float* __restrict__ g,
+                                                    const float* __restrict__ b,
+                                                    T* __restrict__ out) {
   constexpr int d = Q * 256;
   int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   int lane = threadIdx.x & 63;
   if (row >= rows) return;
   float* xr = x + (int64_t)row * d;
-  float4 v[Q];
-  float s = 0.f;
+  float4 v[Q], t[Q], gg[Q], bb[Q];
 #pragma unroll
   for (int i = 0; i < Q; ++i) {
     const int e = (lane + 64 * i) * 4;
     v[i] = *(const float4*)(xr + e);
+    if constexpr (RES) t[i] = ld4<T>(y + (int64_t)row * d + e);
+  }
+#pragma unroll
+  for (int i = 0; i < Q; ++i) {
+    const int e = (lane + 64 * i) * 4;
+    gg[i] = *(const float4*)(g + e);
+    bb[i] = *(const float4*)(b + e);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < Q; ++i) {
     if constexpr (RES) {
-      const float4 t = ld4<T>(y + (int64_t)row * d + e);
-      v[i] = make_float4(v[i].x + t.x, v[i].y + t.y, v[i].z + t.z, v[i].w + t.w);
-      *(float4*)(xr + e) = v[i];
+      v[i] = make_float4(v[i].x + t[i].x, v[i].y + t[i].y, v[i].z + t[i].z, v[i].w + t[i].w);
+      *(float4*)(xr + (lane + 64 * i) * 4) = v[i];
     }
     s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
   }
-  float mean = wave_sum(s) * (1.0f / d);
+  float mean = wave_sum_lanes(s) * (1.0f / d);
   float q = 0.f;
 #pragma unroll
   for (int i = 0; i < Q; ++i) {
     v[i] = make_float4(v[i].x - mean, v[i].y - mean, v[i].z - mean, v[i].w - mean);
     q += (v[i].x * v[i].x + v[i].y * v[i].y) + (v[i].z * v[i].z + v[i].w * v[i].w);
   }
-  float rstd = rsqrtf(wave_sum(q) * (1.0f / d) + 1e-5f);
+  float rstd = rsqrtf(wave_sum_lanes(q) * (1.0f / d) + 1e-5f);
   T* o = out + (int64_t)row * d;
 #pragma unroll
   for (int i = 0; i < Q; ++i) {
     const int e = (lane + 64 * i) * 4;
-    const float4 gg = *(const float4*)(g + e), bb = *(const float4*)(b + e);
-    st4<T>(o + e, make_float4(v[i].x * rstd * gg.x + bb.x, v[i].y * rstd * gg.y + bb.y,
-                              v[i].z * rstd * gg.z + bb.z, v[i].w * rstd * gg.w + bb.w));
+    st4<T>(o + e, make_float4(v[i].x * rstd * gg[i].x + bb[i].x, v[i].y * rstd * gg[i].y + bb[i].y,
+                              v[i].z * rstd * gg[i].z + bb[i].z, v[i].w * rstd * gg[i].w + bb[i].w));
   }
 }
 
