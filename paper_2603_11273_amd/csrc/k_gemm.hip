@@ -849,7 +849,61 @@ __device__ __forceinline__ void epi_wave_half(const Epilogue& e, f32x16 (&acc)[F
 // eight-column run never splits since heads are 64 wide.  No LDS round trip:
 // the store stream issues as fast as the accumulators convert.
 template <int KIND>
-constexpr bool kDirectEpi = KIND == EPI_STORE || KIND == EPI_GELU || KIND == EPI_XKV;
+constexpr bool kDirectEpi =
+    KIND == EPI_STORE || KIND == EPI_GELU || KIND == EPI_XKV || KIND == EPI_QKV;
+
+// V columns of the fused QKV product from the transposed layout: there the
+// MFMA output block is V^T itself (rows = V columns, columns = positions), so
+// it goes through the wave's 16-row LDS stage as the plain epilogue does and
+// is read back as four consecutive positions of one V column -- eight
+// contiguous bytes of V^T[clip][head][dim][position] (1500 is a multiple of
+// 4, so the four never straddle clips); eight lanes fill 64 contiguous bytes.
+template <int FM, int FN>
+__device__ __forceinline__ void epi_direct_vt(const Epilogue& e, f32x16 (&acc)[FM][FN],
+                                              float* stage, int m0w, int n0w, int M, int N,
+                                              int lane) {
+  typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+  const int l32 = lane & 31, lh = lane >> 5;
+  const int n_clips = (M + kCtx - 1) / kCtx;
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      e.out2, (short)0, (int)((int64_t)n_clips * e.n_head * kHeadDim * kVtLd * 2), 0x00020000);
+  const int c4 = (lane & 7) * 4, r8 = lane >> 3;
+  float bv[FN][2][2];     // bias of the lane's V column per (block column, half, it)
+#pragma unroll
+  for (int j = 0; j < FN; ++j)
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int it = 0; it < 2; ++it) bv[j][h][it] = bias1(e, n0w + j * 32 + h * 16 + it * 8 + r8, N);
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int row = m0w + i * 32 + c4;                   // first of four positions
+    const int g = row / kCtx, t = row - g * kCtx;
+    const int rbase = g * e.n_head * kHeadDim * kVtLd + t;
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int r = 0; r < 8; ++r)
+          stage[((r >> 2) * 8 + lh * 4 + (r & 3)) * kStageLd + l32] = acc[i][j][h * 8 + r];
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int it = 0; it < 2; ++it) {
+          const int rr = it * 8 + r8, n = n0w + j * 32 + h * 16 + rr;
+          const float4 v = *(const float4*)&stage[rr * kStageLd + c4];
+          const float bb = bv[j][h][it];
+          const int hd = n - 2 * e.d_model;
+          const u32x2 x = {pack2_bf16(v.x + bb, v.y + bb), pack2_bf16(v.z + bb, v.w + bb)};
+          const uint32_t off = row < M && n < N
+                                   ? (uint32_t)(rbase + ((hd >> 6) * kHeadDim + (hd & 63)) * kVtLd) * 2u
+                                   : 0x80000000u;
+          __builtin_amdgcn_raw_buffer_store_b64(x, rs, off, 0, 0);
+        }
+        __builtin_amdgcn_wave_barrier();
+      }
+  }
+}
 
 template <int KIND, int FM, int FN>
 __device__ __forceinline__ void epi_direct(const Epilogue& e, f32x16 (&acc)[FM][FN], int m0w,
@@ -892,6 +946,14 @@ __device__ __forceinline__ void epi_direct(const Epilogue& e, f32x16 (&acc)[FM][
       if constexpr (KIND == EPI_GELU) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) v[r] = gelu_erf(v[r]);
+      }
+      if constexpr (KIND == EPI_QKV) {
+        // q columns (n < d, whole quads) carry the attention scale into exp2
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (n0w + j * 32 + 8 * q + 4 * lh < e.d_model)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[4 * q + r] *= kQScaleLog2;
       }
       {
         uint32_t o[8];
@@ -1039,6 +1101,19 @@ void k_gemm_bf16_ps(AView a,
   wait_vm_lgkm0_rt<LPT*(S - 1)>(LPT * min(S - 1, total - 1));
   __builtin_amdgcn_s_barrier();
   PS_READ(0, 0, 0);
+  // QKV: output tiles of V columns take the staged V^T epilogue, q / k tiles
+  // the register one; 2 d_model is a multiple of the tile width, so a tile
+  // never mixes them
+  auto vt_of = [&](int t) {
+    if constexpr (KIND != EPI_QKV) {
+      return false;
+    } else {
+      int tm, tn;
+      tile_of((int)blockIdx.x + t * grid, n_tiles, n_tm, n_tn, gm, tm, tn);
+      return tn * BN >= 2 * e.d_model;
+    }
+  };
+  bool tile_vt = vt_of(0);
   int ti = 0, kt = 0;
   for (int gi = 0; gi < total; ++gi) {
     const bool last_k = kt == nk - 1;
@@ -1072,7 +1147,13 @@ void k_gemm_bf16_ps(AView a,
       }
       int tm, tn;
       tile_of((int)blockIdx.x + ti * grid, n_tiles, n_tm, n_tn, gm, tm, tn);
-      if constexpr (SW)
+      if constexpr (SW && KIND == EPI_QKV) {
+        if (tile_vt)
+          epi_direct_vt<FM, FN>(e, acc, (float*)(smem + S * STAGE) + wave * 16 * kStageLd,
+                                tm * BM + wm * TM, tn * BN + wn * TN, M, N, lane);
+        else
+          epi_direct<KIND, FM, FN>(e, acc, tm * BM + wm * TM, tn * BN + wn * TN, M, N, lane);
+      } else if constexpr (SW)
         epi_direct<KIND, FM, FN>(e, acc, tm * BM + wm * TM, tn * BN + wn * TN, M, N, lane);
       else
         epi_wave_half<KIND, FM, FN>(e, acc, (float*)(smem + S * STAGE) + wave * 16 * kStageLd,
@@ -1089,6 +1170,7 @@ void k_gemm_bf16_ps(AView a,
       }
       ++ti;
       kt = 0;
+      tile_vt = vt_of(ti);
     } else {
       ++kt;
     }
@@ -1105,7 +1187,7 @@ template <int BM, int BN, int BK, int WM, int WN, int S, int KIND, int OCC = 1, 
 static void launch_gemm_ps(const AView& a, const bf16_t* w, int M, int N, int K,
                            const Epilogue& e, hipStream_t s, int gm) {
   constexpr size_t lds = (size_t)S * (BM + BN) * BK * sizeof(bf16_t) +
-                        (SW ? 0 : (size_t)WM * WN * 16 * kStageLd * sizeof(float));
+                        (SW && KIND != EPI_QKV ? 0 : (size_t)WM * WN * 16 * kStageLd * sizeof(float));
   auto kfn = k_gemm_bf16_ps<BM, BN, BK, WM, WN, S, KIND, SW>;
   static bool attr = false;
   static int n_cu = 0;
@@ -1130,6 +1212,13 @@ static void launch_gemm_ps(const AView& a, const bf16_t* w, int M, int N, int K,
 static bool direct_epi_ok(const Epilogue& e, int M, int N) {
   if (N % 8 != 0 || ((uintptr_t)e.out & 15) != 0) return false;
   if (e.kind == EPI_XKV) return e.d_model % 64 == 0 && e.slot_stride % 8 == 0;
+  if (e.kind == EPI_QKV) {
+    // tiles of 256 columns never mix q / k with V; V^T fits a buffer resource
+    const int64_t vt_bytes = (int64_t)((M + kCtx - 1) / kCtx) * e.n_head * kHeadDim * kVtLd * 2;
+    if (e.d_model % 128 != 0 || N != 3 * e.d_model || ((uintptr_t)e.out2 & 7) != 0 ||
+        vt_bytes >= (int64_t)INT32_MAX)
+      return false;
+  }
   return e.ldc % 8 == 0 && e.ldc >= N && (int64_t)M * e.ldc * 2 < (int64_t)INT32_MAX;
 }
 
@@ -1212,11 +1301,11 @@ static void launch_gemm_bf16(const AView& a, const bf16_t* w, int M, int N, int 
     else
       launch_gemm_cfg<128, 128, 32, 2, 2, KIND>(a, w, M, N, K, e, s, 8);
   } else if (K % 64 == 0 && t256x256 >= 512) {
-    // (the scatter epilogues of the stem and of the fused QKV product run
-    // slower from the persistent kernel's half-block stage than from the
-    // plain kernel's full-block one)
-    if (KIND != EPI_QKV && KIND != EPI_CONV1 &&
-        fits_u32_offsets(a, M, N, K)) {
+    // (the stem's scatter epilogue runs slower from the persistent kernel's
+    // half-block stage than from the plain kernel's full-block one; the
+    // fused QKV product goes persistent only with its register epilogue)
+    if (KIND != EPI_CONV1 && fits_u32_offsets(a, M, N, K) &&
+        (KIND != EPI_QKV || direct_epi_ok(e, M, N))) {
       const int gm = N >= 3072 ? 8 : 4;
       if constexpr (kDirectEpi<KIND>) {
         if (direct_epi_ok(e, M, N)) {
