@@ -226,3 +226,34 @@ def test_step_errors():
     assert e.value.status == asr.ASR_EFULL
     ctx.release_slot(s)
     assert int(ctx.step(prefill_ids=[3])["slot_of"][0]) == s
+
+
+def test_persistent_gemm_row_tails():
+    """17 clips (25500 rows, 99.6 row tiles of 256) at Whisper-base widths in
+    bf16: the fused QKV and FC1 products are large enough for the persistent
+    GEMM with its register epilogues, and the last row tile is partial, so the
+    out-of-range rows must be dropped.  Clips 0 and 16 (the one holding the
+    partial tile) follow the oracle; so do the cross K/V projected into slots
+    0 and 16 from 17 encoder outputs (one 25500 x 2048 product)."""
+    shape = synth.reduced_shape(synth.SHAPES["base"], 1, 2)
+    seed = 20260360
+    n = 17
+    ctx = make_context(shape, seed, max_slots=n, max_prefill=n, max_decode=0)
+    clips = _clips(seed, [16000 + 7919 * i for i in range(n)])
+    got = ctx.debug_encode(clips)
+    P = cpu_params(shape, seed)
+    for i in (0, n - 1):
+        ref = oracle_encode(clips[i], P, shape)
+        e = rel_err(got[i], ref)
+        print(f"row-tail encoder clip {i}: rel err {e:.3e}")
+        assert e <= TOL["bf16"]
+    E = np.stack([synth.encoder_output(seed, b, shape.d_model).numpy() for b in range(n)])
+    ctx.debug_set_encoder_out(list(range(n)), [-1] * n, [1] * n, E)
+    for b in (0, n - 1):
+        ckv = OW.cross_kv(E[b].astype(np.float64), P, shape.n_dec)
+        cx = ctx.debug_get_kv(b, 1)
+        for l in range(shape.n_dec):
+            for kv in range(2):
+                ref = ckv[l][kv].reshape(1500, shape.n_head, 64).transpose(1, 0, 2)
+                e = rel_err(cx[l, kv], ref)
+                assert e <= TOL["bf16"], (b, l, kv, e)
