@@ -83,8 +83,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
       rv[u] = *(const uint4*)(vbase + (int64_t)row * kVtLd + (k0) + ch * 8);        \
     }                                                                               \
   } while (0)
-  // V^T rows 16..31 (mod 32) keep their two 8-byte halves swapped, so the
-  // 8-byte fragment reads of 32 consecutive rows hit distinct banks
+  // V^T rows keep their two 8-byte halves swapped when bit 4 XOR bit 5 of
+  // the row is set: the 8-byte fragment reads of 32 consecutive rows then hit
+  // distinct banks, and a lane's reads of rows r and r + 32 are never a
+  // whole number of 512-byte steps apart (the compiler would pair such reads
+  // into one two-address instruction whose halves share banks)
 #define FA_SSTORE(buf)                                                              \
   do {                                                                              \
     _Pragma("unroll") for (int u = 0; u < CPT; ++u) {                               \
@@ -92,7 +95,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
       const int pos = row * 64 + ((ch ^ fa_swz(row)) * 8);                          \
       *(uint4*)&Ks[buf][pos] = rk[u];                                               \
       const uint4 v = rv[u];                                                        \
-      *(uint4*)&Vs[buf][pos] = (row & 16) ? uint4{v.z, v.w, v.x, v.y} : v;          \
+      *(uint4*)&Vs[buf][pos] = (((row >> 4) ^ (row >> 5)) & 1) ? uint4{v.z, v.w, v.x, v.y} : v; \
     }                                                                               \
   } while (0)
 
@@ -214,8 +217,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
         const bf16_t* v1 = Vc + (32 + l32) * 64;
         const uint2 a0 = *(const uint2*)(v0 + ((c ^ sw) * 8) + vhalf);
         const uint2 a1 = *(const uint2*)(v0 + (((c + 1) ^ sw) * 8) + vhalf);
-        const uint2 c0 = *(const uint2*)(v1 + ((c ^ sw) * 8) + vhalf);
-        const uint2 c1 = *(const uint2*)(v1 + (((c + 1) ^ sw) * 8) + vhalf);
+        const uint2 c0 = *(const uint2*)(v1 + ((c ^ sw) * 8) + (vhalf ^ 4));
+        const uint2 c1 = *(const uint2*)(v1 + (((c + 1) ^ sw) * 8) + (vhalf ^ 4));
         o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(uint4{a0.x, a0.y, a1.x, a1.y}),
                                                      pb[kb][hf], o0, 0, 0, 0);
         o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(uint4{c0.x, c0.y, c1.x, c1.y}),
