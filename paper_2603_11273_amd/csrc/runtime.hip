@@ -117,6 +117,10 @@ struct asr_ctx {
   int overlap_reserve = 0;          // CUs its persistent GEMMs leave to the decode rows
   hipStream_t pstream = nullptr;    // that stream (non-blocking, default priority)
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  // the encoder's second clip group runs its layers on estream beside the
+  // first (non-blocking, default priority)
+  hipStream_t estream = nullptr;
+  hipEvent_t ev_efork = nullptr, ev_ejoin = nullptr;
   std::unordered_map<int64_t, Request> serving;   // admitted, not finished (audio kept
                                                   // for a re-prefill after preemption)
   Layout L;
@@ -568,77 +572,113 @@ asr_status encode_clips(asr_ctx* c, int n) {
     e.pos = c->at<float>(L.sinus);
     gemm_any<T>(c, a, L.conv2_w, n * kCtx, d, 3 * d, e);
   }
-  const int R = n * kCtx;
-  float* x = c->at<float>(L.x);
-  T* xn = c->at<T>(L.xn);
-  T* qkv = c->at<T>(L.qkv);
-  T* att = c->at<T>(L.att);
-  T* hid = c->at<T>(L.hid);
-  // The residual branches (attention out-projection, FC2) are written in the
-  // storage type to y, which borrows the QKV buffer (dead once attention has
-  // run); the LayerNorm kernel that follows adds y into the float32 stream,
-  // as a model stored in bf16 adds its bf16 branch outputs to the residual.
-  T* y = c->at<T>(L.qkv);
-  if (g.n_enc > 0) ln_any<T>(c, x, R, L.enc[0].ln1_g, L.enc[0].ln1_b, xn);
-  for (int l = 0; l < g.n_enc; ++l) {
-    const EncLayer& w = L.enc[l];
-    // xn holds LN_1(x) here
-    {
-      // bf16: q, k into the fused buffer and v transposed per head for the
-      // flash-attention kernel; fp32: plain [R][3d]
-      AView a{xn, d, 0, R};
-      Epilogue e{};
-      e.kind = c->bf16() ? EPI_QKV : EPI_STORE;
-      e.out = qkv;
-      e.ldc = 3 * d;
-      e.bias = c->at<float>(w.qkv_b);
-      e.d_model = d;
-      e.n_head = H;
-      e.out2 = c->at(L.vt);
-      gemm_any<T>(c, a, w.qkv_w, R, 3 * d, d, e);
+  float* x_all = c->at<float>(L.x);
+  T* xn_all = c->at<T>(L.xn);
+  T* qkv_all = c->at<T>(L.qkv);
+  T* att_all = c->at<T>(L.att);
+  T* hid_all = c->at<T>(L.hid);
+  // The clips split into two groups whose layer chains run on two streams:
+  // while one group's memory-bound LayerNorm or the last partial round of a
+  // persistent GEMM runs, the other group's kernels fill the idle CUs.  The
+  // groups own disjoint rows of every buffer.
+  const int G = n >= 2 && g.n_enc > 0 ? 2 : 1;
+  hipStream_t main_stream = c->stream;
+  if (G == 2) {
+    if (!c->estream) {
+      HIPCHK(hipStreamCreateWithFlags(&c->estream, hipStreamNonBlocking));
+      HIPCHK(hipEventCreateWithFlags(&c->ev_efork, hipEventDisableTiming));
+      HIPCHK(hipEventCreateWithFlags(&c->ev_ejoin, hipEventDisableTiming));
     }
-    timed(c, ASR_K_ATTN, 4.0 * n * H * (double)kCtx * kCtx * 64,
-          (double)R * 4 * d * c->es, [&] {
-            if (c->bf16())
-              flash_attn_bf16((const bf16_t*)qkv, c->at<bf16_t>(L.vt), (bf16_t*)att, n, H,
-                              c->stream);
-            else
-              flash_attn_f32((const float*)qkv, (float*)att, n, H, c->stream);
-          });
-    {
-      AView a{att, d, 0, R};
-      Epilogue e{};
-      e.kind = EPI_STORE;
-      e.out = y;
-      e.ldc = d;
-      e.bias = c->at<float>(w.o_b);
-      gemm_any<T>(c, a, w.o_w, R, d, d, e);
-    }
-    res_ln_any<T>(c, x, y, R, w.ln2_g, w.ln2_b, xn);
-    {
-      AView a{xn, d, 0, R};
-      Epilogue e{};
-      e.kind = EPI_GELU;
-      e.out = hid;
-      e.ldc = F;
-      e.bias = c->at<float>(w.fc1_b);
-      gemm_any<T>(c, a, w.fc1_w, R, F, d, e);
-    }
-    {
-      AView a{hid, F, 0, R};
-      Epilogue e{};
-      e.kind = EPI_STORE;
-      e.out = y;
-      e.ldc = d;
-      e.bias = c->at<float>(w.fc2_b);
-      gemm_any<T>(c, a, w.fc2_w, R, d, F, e);
-    }
-    // the next LayerNorm: the next layer's LN_1, or ln_post after the last layer
-    const bool last = l + 1 == g.n_enc;
-    res_ln_any<T>(c, x, y, R, last ? L.lnp_g : L.enc[l + 1].ln1_g,
-                  last ? L.lnp_b : L.enc[l + 1].ln1_b, xn);
+    HIPCHK(hipEventRecord(c->ev_efork, main_stream));
+    HIPCHK(hipStreamWaitEvent(c->estream, c->ev_efork, 0));
   }
-  if (g.n_enc == 0) ln_any<T>(c, x, R, L.lnp_g, L.lnp_b, xn);
+  int clip0[2] = {0, n / 2}, nclip[2] = {G == 2 ? n / 2 : n, n - n / 2};
+  for (int l = 0; l <= g.n_enc; ++l) {
+    for (int grp = 0; grp < G; ++grp) {
+      c->stream = grp == 0 ? main_stream : c->estream;
+      const int ng = nclip[grp], R = ng * kCtx;
+      const int64_t r0 = (int64_t)clip0[grp] * kCtx;
+      float* x = x_all + r0 * d;
+      T* xn = xn_all + r0 * d;
+      T* qkv = qkv_all + r0 * 3 * d;
+      T* att = att_all + r0 * d;
+      T* hid = hid_all + r0 * F;
+      // The residual branches (attention out-projection, FC2) are written in
+      // the storage type to y, which borrows the group's QKV rows (dead once
+      // attention has run); the LayerNorm kernel that follows adds y into the
+      // float32 stream, as a model stored in bf16 adds its bf16 branch
+      // outputs to the residual.
+      T* y = qkv;
+      if (l == 0) {
+        ln_any<T>(c, x, R, L.enc[0].ln1_g, L.enc[0].ln1_b, xn);
+        continue;
+      }
+      const EncLayer& w = L.enc[l - 1];
+      // xn holds LN_1(x) here
+      {
+        // bf16: q, k into the fused buffer and v transposed per head for the
+        // flash-attention kernel; fp32: plain [R][3d]
+        AView a{xn, d, 0, R};
+        Epilogue e{};
+        e.kind = c->bf16() ? EPI_QKV : EPI_STORE;
+        e.out = qkv;
+        e.ldc = 3 * d;
+        e.bias = c->at<float>(w.qkv_b);
+        e.d_model = d;
+        e.n_head = H;
+        e.out2 = c->bf16() ? (void*)(c->at<T>(L.vt) + (int64_t)clip0[grp] * H * kHeadDim * kVtLd)
+                           : nullptr;
+        gemm_any<T>(c, a, w.qkv_w, R, 3 * d, d, e);
+      }
+      timed(c, ASR_K_ATTN, 4.0 * ng * H * (double)kCtx * kCtx * 64,
+            (double)R * 4 * d * c->es, [&] {
+              if (c->bf16())
+                flash_attn_bf16((const bf16_t*)qkv,
+                                c->at<bf16_t>(L.vt) + (int64_t)clip0[grp] * H * kHeadDim * kVtLd,
+                                (bf16_t*)att, ng, H, c->stream);
+              else
+                flash_attn_f32((const float*)qkv, (float*)att, ng, H, c->stream);
+            });
+      {
+        AView a{att, d, 0, R};
+        Epilogue e{};
+        e.kind = EPI_STORE;
+        e.out = y;
+        e.ldc = d;
+        e.bias = c->at<float>(w.o_b);
+        gemm_any<T>(c, a, w.o_w, R, d, d, e);
+      }
+      res_ln_any<T>(c, x, y, R, w.ln2_g, w.ln2_b, xn);
+      {
+        AView a{xn, d, 0, R};
+        Epilogue e{};
+        e.kind = EPI_GELU;
+        e.out = hid;
+        e.ldc = F;
+        e.bias = c->at<float>(w.fc1_b);
+        gemm_any<T>(c, a, w.fc1_w, R, F, d, e);
+      }
+      {
+        AView a{hid, F, 0, R};
+        Epilogue e{};
+        e.kind = EPI_STORE;
+        e.out = y;
+        e.ldc = d;
+        e.bias = c->at<float>(w.fc2_b);
+        gemm_any<T>(c, a, w.fc2_w, R, d, F, e);
+      }
+      // the next LayerNorm: the next layer's LN_1, or ln_post after the last layer
+      const bool last = l == g.n_enc;
+      res_ln_any<T>(c, x, y, R, last ? L.lnp_g : L.enc[l].ln1_g,
+                    last ? L.lnp_b : L.enc[l].ln1_b, xn);
+    }
+  }
+  c->stream = main_stream;
+  if (G == 2) {
+    HIPCHK(hipEventRecord(c->ev_ejoin, c->estream));
+    HIPCHK(hipStreamWaitEvent(main_stream, c->ev_ejoin, 0));
+  }
+  if (g.n_enc == 0) ln_any<T>(c, x_all, n * kCtx, L.lnp_g, L.lnp_b, xn_all);
   CHECK_LAUNCH();
   return ASR_OK;
 }
@@ -852,6 +892,10 @@ asr_status asr_destroy(asr_ctx* c) {
     if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
     if (c->ev_join) (void)hipEventDestroy(c->ev_join);
     if (c->pstream) (void)hipStreamDestroy(c->pstream);
+    if (c->estream) (void)hipStreamSynchronize(c->estream);
+    if (c->ev_efork) (void)hipEventDestroy(c->ev_efork);
+    if (c->ev_ejoin) (void)hipEventDestroy(c->ev_ejoin);
+    if (c->estream) (void)hipStreamDestroy(c->estream);
   }
   delete c;
   return ASR_OK;
