@@ -302,6 +302,14 @@ asr_status asr_serve_simulate(asr_ctx* ctx, const asr_sim_cost* cost, int64_t t0
                               int32_t* n_tokens, int32_t* n_preempt, int64_t* token_us,
                               int64_t token_cap, int64_t* t_end_us);
 
+/* Prefill clips split into n groups (1..4, default 2) whose encoder layers
+ * run on n streams (the context's stream and n-1 of its own, default
+ * priority), so one group's memory-bound LayerNorms and the last partial
+ * round of a GEMM overlap another group's kernels; n = 1 runs the encoder as
+ * one chain, where every launch owns the GPU (what per-kernel timing needs).
+ * Results do not depend on n. */
+asr_status asr_set_encoder_streams(asr_ctx* ctx, int32_t n);
+
 /* classes is a bit mask over the asr_kernel_class values: bit k selects class
  * k, 0 turns timing off, ASR_TIME_ALL times every class.  An event pair is
  * recorded on the context's stream around every launch (and phase) of a

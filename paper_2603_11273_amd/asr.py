@@ -27,7 +27,8 @@ EXPORTED = [
     "asr_create", "asr_destroy", "asr_last_error", "asr_workspace_size", "asr_bind",
     "asr_n_params", "asr_param_numel", "asr_load_weights", "asr_set_policy", "asr_submit",
     "asr_rank", "asr_pop_batch", "asr_queue_len", "asr_step", "asr_release_slot",
-    "asr_slot_info", "asr_set_timing", "asr_get_timing", "asr_reset_timing",
+    "asr_slot_info", "asr_set_encoder_streams", "asr_set_timing", "asr_get_timing",
+    "asr_reset_timing",
     "asr_debug_logmel", "asr_debug_encode", "asr_debug_attention", "asr_debug_set_encoder_out",
     "asr_debug_get_kv",
     "asr_debug_set_self_kv", "asr_serve_config", "asr_serve_step", "asr_serve_plan",
@@ -110,6 +111,7 @@ def _load():
         "asr_step": [vp, P(StepIn), P(StepOut)],
         "asr_release_slot": [vp, i32],
         "asr_slot_info": [vp, i32, P(i32), P(i64), P(i32), P(i32)],
+        "asr_set_encoder_streams": [vp, i32],
         "asr_set_timing": [vp, i32],
         "asr_get_timing": [vp, i32, P(C.c_double), P(i64), P(C.c_double), P(C.c_double)],
         "asr_reset_timing": [vp],
@@ -368,6 +370,10 @@ class Context:
                                  C.byref(left)))
         return {"occupied": bool(occ.value), "id": rid.value, "position": pos.value,
                 "steps_left": left.value}
+
+    def set_encoder_streams(self, n):
+        """Prefill clips in n groups whose encoder layers run on n streams."""
+        _check(lib.asr_set_encoder_streams(self.h, int(n)))
 
     # -- timing ---------------------------------------------------------------
     def set_timing(self, classes=True):

@@ -117,10 +117,12 @@ struct asr_ctx {
   int overlap_reserve = 0;          // CUs its persistent GEMMs leave to the decode rows
   hipStream_t pstream = nullptr;    // that stream (non-blocking, default priority)
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
-  // the encoder's second clip group runs its layers on estream beside the
-  // first (non-blocking, default priority)
-  hipStream_t estream = nullptr;
-  hipEvent_t ev_efork = nullptr, ev_ejoin = nullptr;
+  // the encoder's clips split into enc_groups groups; groups after the first
+  // run their layers on estream[] beside it (non-blocking, default priority)
+  static constexpr int kEncGroups = 4;
+  int enc_groups = 2;
+  hipStream_t estream[kEncGroups - 1] = {};
+  hipEvent_t ev_efork = nullptr, ev_ejoin[kEncGroups - 1] = {};
   std::unordered_map<int64_t, Request> serving;   // admitted, not finished (audio kept
                                                   // for a re-prefill after preemption)
   Layout L;
@@ -577,25 +579,31 @@ asr_status encode_clips(asr_ctx* c, int n) {
   T* qkv_all = c->at<T>(L.qkv);
   T* att_all = c->at<T>(L.att);
   T* hid_all = c->at<T>(L.hid);
-  // The clips split into two groups whose layer chains run on two streams:
-  // while one group's memory-bound LayerNorm or the last partial round of a
-  // persistent GEMM runs, the other group's kernels fill the idle CUs.  The
-  // groups own disjoint rows of every buffer.
-  const int G = n >= 2 && g.n_enc > 0 ? 2 : 1;
+  // The clips split into groups (two by default) whose layer chains run on
+  // their own streams: while one group's memory-bound LayerNorm or the last
+  // partial round of a persistent GEMM runs, another group's kernels fill the
+  // idle CUs.  The groups own disjoint rows of every buffer.
+  const int G = g.n_enc > 0 ? std::max(1, std::min(n, c->enc_groups)) : 1;
   hipStream_t main_stream = c->stream;
-  if (G == 2) {
-    if (!c->estream) {
-      HIPCHK(hipStreamCreateWithFlags(&c->estream, hipStreamNonBlocking));
+  if (G > 1) {
+    if (!c->ev_efork) {
       HIPCHK(hipEventCreateWithFlags(&c->ev_efork, hipEventDisableTiming));
-      HIPCHK(hipEventCreateWithFlags(&c->ev_ejoin, hipEventDisableTiming));
+      for (int i = 0; i < asr_ctx::kEncGroups - 1; ++i) {
+        HIPCHK(hipStreamCreateWithFlags(&c->estream[i], hipStreamNonBlocking));
+        HIPCHK(hipEventCreateWithFlags(&c->ev_ejoin[i], hipEventDisableTiming));
+      }
     }
     HIPCHK(hipEventRecord(c->ev_efork, main_stream));
-    HIPCHK(hipStreamWaitEvent(c->estream, c->ev_efork, 0));
+    for (int i = 0; i < G - 1; ++i) HIPCHK(hipStreamWaitEvent(c->estream[i], c->ev_efork, 0));
   }
-  int clip0[2] = {0, n / 2}, nclip[2] = {G == 2 ? n / 2 : n, n - n / 2};
+  int clip0[asr_ctx::kEncGroups], nclip[asr_ctx::kEncGroups];
+  for (int i = 0; i < G; ++i) {
+    clip0[i] = n * i / G;
+    nclip[i] = n * (i + 1) / G - clip0[i];
+  }
   for (int l = 0; l <= g.n_enc; ++l) {
     for (int grp = 0; grp < G; ++grp) {
-      c->stream = grp == 0 ? main_stream : c->estream;
+      c->stream = grp == 0 ? main_stream : c->estream[grp - 1];
       const int ng = nclip[grp], R = ng * kCtx;
       const int64_t r0 = (int64_t)clip0[grp] * kCtx;
       float* x = x_all + r0 * d;
@@ -674,9 +682,9 @@ asr_status encode_clips(asr_ctx* c, int n) {
     }
   }
   c->stream = main_stream;
-  if (G == 2) {
-    HIPCHK(hipEventRecord(c->ev_ejoin, c->estream));
-    HIPCHK(hipStreamWaitEvent(main_stream, c->ev_ejoin, 0));
+  for (int i = 0; i < G - 1; ++i) {
+    HIPCHK(hipEventRecord(c->ev_ejoin[i], c->estream[i]));
+    HIPCHK(hipStreamWaitEvent(main_stream, c->ev_ejoin[i], 0));
   }
   if (g.n_enc == 0) ln_any<T>(c, x_all, n * kCtx, L.lnp_g, L.lnp_b, xn_all);
   CHECK_LAUNCH();
@@ -892,10 +900,12 @@ asr_status asr_destroy(asr_ctx* c) {
     if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
     if (c->ev_join) (void)hipEventDestroy(c->ev_join);
     if (c->pstream) (void)hipStreamDestroy(c->pstream);
-    if (c->estream) (void)hipStreamSynchronize(c->estream);
+    for (int i = 0; i < asr_ctx::kEncGroups - 1; ++i) {
+      if (c->estream[i]) (void)hipStreamSynchronize(c->estream[i]);
+      if (c->ev_ejoin[i]) (void)hipEventDestroy(c->ev_ejoin[i]);
+      if (c->estream[i]) (void)hipStreamDestroy(c->estream[i]);
+    }
     if (c->ev_efork) (void)hipEventDestroy(c->ev_efork);
-    if (c->ev_ejoin) (void)hipEventDestroy(c->ev_ejoin);
-    if (c->estream) (void)hipStreamDestroy(c->estream);
   }
   delete c;
   return ASR_OK;
@@ -1496,6 +1506,13 @@ asr_status asr_serve_tokens(asr_ctx* c, int64_t id, int32_t* tokens, int32_t cap
   if ((int32_t)t.size() > cap) return fail(ASR_EINVAL, "token buffer too small");
   for (size_t i = 0; i < t.size(); ++i) tokens[i] = t[i];
   *n = (int32_t)t.size();
+  return ASR_OK;
+}
+
+asr_status asr_set_encoder_streams(asr_ctx* c, int32_t n) {
+  if (!c) return fail(ASR_EINVAL, "NULL context");
+  if (n < 1 || n > asr_ctx::kEncGroups) return fail(ASR_EINVAL, "n out of [1, 4]");
+  c->enc_groups = n;
   return ASR_OK;
 }
 
