@@ -35,7 +35,9 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "gemm_bf16_large-v3_step_traffic.md")
-GEMM_SOURCE = os.path.join(ROOT, "paper_2603_11273_amd", "csrc", "k_gemm.hip")
+# the GEMM kernels and the device helpers their epilogues inline
+GEMM_SOURCES = [os.path.join(ROOT, "paper_2603_11273_amd", "csrc", f)
+                for f in ("k_gemm.hip", "asr_device.h", "asr_kernels.h")]
 
 
 def gemm_traffic_per_launch():
@@ -46,7 +48,10 @@ def gemm_traffic_per_launch():
     try:
         text = open(TRAFFIC_SUMMARY).read()
         rec = json.loads(re.search(r"```json\n(.*?)\n```", text, re.S).group(1))
-        sha = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()[:16]
+        h = hashlib.sha256()
+        for f in GEMM_SOURCES:
+            h.update(open(f, "rb").read())
+        sha = h.hexdigest()[:16]
     except Exception:
         return None
     return rec["gemm_bytes_per_launch"] if rec.get("kernel_source_sha256_16") == sha else None

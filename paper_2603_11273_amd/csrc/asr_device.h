@@ -38,23 +38,25 @@ struct St<bf16_t> {
   static __device__ __forceinline__ void st(bf16_t* p, int64_t i, float v) { p[i] = f2bf(v); }
 };
 
-// GELU(x) = x/2 (1 + erf(x / sqrt 2)) with erf from Abramowitz & Stegun
-// 7.1.26 (Hastings' rational approximation, |error| <= 1.5e-7 on the erf):
-// for z = |x|/sqrt 2, 1 - erf(z) = q = t (a1 + t (a2 + ... + t a5)) e^{-z^2},
-// t = 1 / (1 + p z).  Then 1 + erf(x/sqrt 2) is 2 - q for x >= 0 and q for
-// x < 0, so the negative tail never subtracts nearly equal numbers.  About
-// fourteen instructions instead of a library erf; the error sits far below
-// the bfloat16 rounding of the products that use it.
+// GELU(x) = x Phi(x), Phi the standard normal CDF, with erf from
+// Abramowitz & Stegun 7.1.26 (Hastings' rational approximation, |error| <=
+// 1.5e-7 on the erf): for z = |x|/sqrt 2, 1 - erf(z) = t (a1 + t (a2 + ... +
+// t a5)) e^{-z^2}, t = 1 / (1 + p z).  Its half is h = Phi(-|x|); GELU(x) is
+// x - x h for x >= 0 and x h for x < 0, so the negative tail never subtracts
+// nearly equal numbers.  The 1/sqrt 2 folds into p, the 1/2 into the a_i and
+// e^{-z^2} = 2^(-x^2 log2(e) / 2): twelve VALU instructions and two
+// transcendentals instead of a library erf; the error sits far below the
+// bfloat16 rounding of the products that use it.
 __device__ __forceinline__ float gelu_erf(float x) {
-  const float z = fabsf(x) * 0.70710678118654752f;
-  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, z, 1.0f));
-  float poly = fmaf(1.061405429f, t, -1.453152027f);
-  poly = fmaf(poly, t, 1.421413741f);
-  poly = fmaf(poly, t, -0.284496736f);
-  poly = fmaf(poly, t, 0.254829592f);
-  poly *= t;
-  const float q = poly * __builtin_amdgcn_exp2f(-z * z * 1.4426950408889634f);
-  return 0.5f * x * (x >= 0.0f ? 2.0f - q : q);
+  const float t =
+      __builtin_amdgcn_rcpf(fmaf(0.3275911f * 0.70710678118654752f, fabsf(x), 1.0f));
+  float poly = fmaf(0.5f * 1.061405429f, t, 0.5f * -1.453152027f);
+  poly = fmaf(poly, t, 0.5f * 1.421413741f);
+  poly = fmaf(poly, t, 0.5f * -0.284496736f);
+  poly = fmaf(poly, t, 0.5f * 0.254829592f);
+  const float h = poly * t * __builtin_amdgcn_exp2f(x * x * (-0.5f * 1.4426950408889634f));
+  const float xh = x * h;
+  return x >= 0.0f ? x - xh : xh;
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
