@@ -541,9 +541,14 @@ void res_ln_any(asr_ctx* c, float* x, const T* y, int rows, size_t g, size_t b, 
   });
 }
 
-// mel -> stem -> encoder layers -> ln_post; E (storage type) ends in L.xn.
 template <typename T>
-asr_status encode_clips(asr_ctx* c, int n) {
+asr_status cross_kv(asr_ctx* c, const void* E, int n, int slot0);
+
+// mel -> stem -> encoder layers -> ln_post (-> with xkv, the cross K/V of
+// every decoder layer into the slots in L.p_slots); E (storage type) ends in
+// L.xn.
+template <typename T>
+asr_status encode_clips(asr_ctx* c, int n, bool xkv = false) {
   const asr_model_cfg& g = c->cfg;
   const int d = g.d_model, F = g.d_ffn, Mm = g.n_mels, H = g.n_head;
   const Layout& L = c->L;
@@ -553,27 +558,6 @@ asr_status encode_clips(asr_ctx* c, int n) {
     mel_normalize<T>(c->at<float>(L.mel_raw), c->at<uint32_t>(L.clip_max), n, Mm,
                      c->at<T>(L.mel_norm), 1, c->stream);
   });
-  // conv1: rows t of clip g read padded mel rows t .. t+2 (positions t-1 .. t+1)
-  {
-    AView a{c->at(L.mel_norm), Mm, (int64_t)(kFrames + 2) * Mm, kFrames};
-    Epilogue e{};
-    e.kind = EPI_CONV1;
-    e.out = c->at(L.h1);
-    e.bias = c->at<float>(L.conv1_b);
-    e.d_model = d;
-    gemm_any<T>(c, a, L.conv1_w, n * kFrames, d, 3 * Mm, e);
-  }
-  // conv2 (stride 2): output t reads h1 rows 2t .. 2t+2 (positions 2t-1 .. 2t+1)
-  {
-    AView a{c->at(L.h1), 2 * (int64_t)d, (int64_t)(kFrames + 1) * d, kCtx};
-    Epilogue e{};
-    e.kind = EPI_CONV2;
-    e.out = c->at(L.x);
-    e.ldc = d;
-    e.bias = c->at<float>(L.conv2_b);
-    e.pos = c->at<float>(L.sinus);
-    gemm_any<T>(c, a, L.conv2_w, n * kCtx, d, 3 * d, e);
-  }
   float* x_all = c->at<float>(L.x);
   T* xn_all = c->at<T>(L.xn);
   T* qkv_all = c->at<T>(L.qkv);
@@ -583,7 +567,7 @@ asr_status encode_clips(asr_ctx* c, int n) {
   // their own streams: while one group's memory-bound LayerNorm or the last
   // partial round of a persistent GEMM runs, another group's kernels fill the
   // idle CUs.  The groups own disjoint rows of every buffer.
-  const int G = g.n_enc > 0 ? std::max(1, std::min(n, c->enc_groups)) : 1;
+  const int G = std::max(1, std::min(n, c->enc_groups));
   hipStream_t main_stream = c->stream;
   if (G > 1) {
     if (!c->ev_efork) {
@@ -618,7 +602,30 @@ asr_status encode_clips(asr_ctx* c, int n) {
       // outputs to the residual.
       T* y = qkv;
       if (l == 0) {
-        ln_any<T>(c, x, R, L.enc[0].ln1_g, L.enc[0].ln1_b, xn);
+        // conv1: rows t of clip g read padded mel rows t .. t+2 (positions t-1 .. t+1)
+        {
+          AView a{c->at<T>(L.mel_norm) + (int64_t)clip0[grp] * (kFrames + 2) * Mm, Mm,
+                  (int64_t)(kFrames + 2) * Mm, kFrames};
+          Epilogue e{};
+          e.kind = EPI_CONV1;
+          e.out = c->at<T>(L.h1) + (int64_t)clip0[grp] * (kFrames + 1) * d;
+          e.bias = c->at<float>(L.conv1_b);
+          e.d_model = d;
+          gemm_any<T>(c, a, L.conv1_w, ng * kFrames, d, 3 * Mm, e);
+        }
+        // conv2 (stride 2): output t reads h1 rows 2t .. 2t+2 (positions 2t-1 .. 2t+1)
+        {
+          AView a{c->at<T>(L.h1) + (int64_t)clip0[grp] * (kFrames + 1) * d, 2 * (int64_t)d,
+                  (int64_t)(kFrames + 1) * d, kCtx};
+          Epilogue e{};
+          e.kind = EPI_CONV2;
+          e.out = x;
+          e.ldc = d;
+          e.bias = c->at<float>(L.conv2_b);
+          e.pos = c->at<float>(L.sinus);
+          gemm_any<T>(c, a, L.conv2_w, R, d, 3 * d, e);
+        }
+        if (g.n_enc > 0) ln_any<T>(c, x, R, L.enc[0].ln1_g, L.enc[0].ln1_b, xn);
         continue;
       }
       const EncLayer& w = L.enc[l - 1];
@@ -679,6 +686,13 @@ asr_status encode_clips(asr_ctx* c, int n) {
       const bool last = l == g.n_enc;
       res_ln_any<T>(c, x, y, R, last ? L.lnp_g : L.enc[l].ln1_g,
                     last ? L.lnp_b : L.enc[l].ln1_b, xn);
+      if (last && xkv) {
+        const asr_status st2 = cross_kv<T>(c, xn, ng, clip0[grp]);
+        if (st2 != ASR_OK) {
+          c->stream = main_stream;
+          return st2;
+        }
+      }
     }
   }
   c->stream = main_stream;
@@ -686,15 +700,21 @@ asr_status encode_clips(asr_ctx* c, int n) {
     HIPCHK(hipEventRecord(c->ev_ejoin[i], c->estream[i]));
     HIPCHK(hipStreamWaitEvent(main_stream, c->ev_ejoin[i], 0));
   }
-  if (g.n_enc == 0) ln_any<T>(c, x_all, n * kCtx, L.lnp_g, L.lnp_b, xn_all);
+  if (g.n_enc == 0) {
+    ln_any<T>(c, x_all, n * kCtx, L.lnp_g, L.lnp_b, xn_all);
+    if (xkv) {
+      const asr_status st2 = cross_kv<T>(c, xn_all, n, 0);
+      if (st2 != ASR_OK) return st2;
+    }
+  }
   CHECK_LAUNCH();
   return ASR_OK;
 }
 
 // Projects E (storage type, [n][1500][d] at `E`) into the cross caches of
-// the slots listed in device array L.p_slots.
+// the slots listed in device array L.p_slots from entry slot0 on.
 template <typename T>
-asr_status cross_kv(asr_ctx* c, const void* E, int n) {
+asr_status cross_kv(asr_ctx* c, const void* E, int n, int slot0) {
   const asr_model_cfg& g = c->cfg;
   const int d = g.d_model;
   AView a{E, d, 0, n * kCtx};
@@ -702,7 +722,7 @@ asr_status cross_kv(asr_ctx* c, const void* E, int n) {
   e.kind = EPI_XKV;
   e.out = c->at(c->L.cross_kv);
   e.bias = c->at<float>(c->L.xkv_b);
-  e.slots = c->at<int32_t>(c->L.p_slots);
+  e.slots = c->at<int32_t>(c->L.p_slots) + slot0;
   e.slot_stride = c->L.cross_stride;
   e.d_model = d;
   e.n_head = g.n_head;
@@ -1120,12 +1140,9 @@ asr_status launch_prefill(asr_ctx* c, const std::vector<const Request*>& reqs,
   HIPCHK(hipMemcpyAsync(c->at(c->L.pcm_n), ns.data(), P * 8, hipMemcpyHostToDevice, s));
   HIPCHK(hipMemcpyAsync(c->at(c->L.p_slots), slots.data(), P * 4, hipMemcpyHostToDevice, s));
   PhaseMark pm(c, ASR_K_PREFILL);
-  asr_status st = c->bf16() ? encode_clips<bf16_t>(c, P) : encode_clips<float>(c, P);
+  const bool xkv = c->cfg.n_dec > 0;
+  asr_status st = c->bf16() ? encode_clips<bf16_t>(c, P, xkv) : encode_clips<float>(c, P, xkv);
   if (st != ASR_OK) return st;
-  if (c->cfg.n_dec > 0) {
-    st = c->bf16() ? cross_kv<bf16_t>(c, c->at(c->L.xn), P) : cross_kv<float>(c, c->at(c->L.xn), P);
-    if (st != ASR_OK) return st;
-  }
   pm.end();
   (void)any_host;
   return ASR_OK;
@@ -1657,7 +1674,7 @@ asr_status asr_debug_set_encoder_out(asr_ctx* c, const int32_t* slots, const int
   else
     convert_from_f32<float>(tmp, c->at<float>(c->L.xn), cnt, s);
   HIPCHK(hipMemcpyAsync(c->at(c->L.p_slots), slots, n * 4, hipMemcpyHostToDevice, s));
-  st = c->bf16() ? cross_kv<bf16_t>(c, c->at(c->L.xn), n) : cross_kv<float>(c, c->at(c->L.xn), n);
+  st = c->bf16() ? cross_kv<bf16_t>(c, c->at(c->L.xn), n, 0) : cross_kv<float>(c, c->at(c->L.xn), n, 0);
   if (st != ASR_OK) return st;
   HIPCHK(hipStreamSynchronize(s));
   for (int i = 0; i < n; ++i) {
