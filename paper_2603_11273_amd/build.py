@@ -1,4 +1,5 @@
-"""Builds the HIP library libasr_mi355x.so in-tree for gfx950 (MI355X).
+"""Builds the HIP library libasr_mi355x.so in-tree for gfx950 (MI355X), and
+the seeded input generator libasr_synth.so (test and benchmark input only).
 
     python -m paper_2603_11273_amd.build
 
@@ -16,6 +17,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libasr_mi355x.so")
+SYNTH_LIB = os.path.join(HERE, "libasr_synth.so")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 
 HIP_SOURCES = ["k_misc.hip", "k_gemm.hip", "k_attn.hip", "runtime.hip"]
@@ -43,6 +45,8 @@ def build(verbose: bool = False) -> str:
     for src in HIP_SOURCES:
         obj = os.path.join(BUILD, src + ".o")
         jobs.append([HIPCC, *HIP_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+    jobs.append([HIPCC, *HIP_FLAGS, "-c", os.path.join(CSRC, "synth_gen.hip"), "-o",
+                 os.path.join(BUILD, "synth_gen.hip.o")])
     for src in CPP_SOURCES:
         obj = os.path.join(BUILD, src + ".o")
         jobs.append(["g++", "-O2", "-std=c++17", "-fPIC", "-Wall", "-c",
@@ -59,6 +63,10 @@ def build(verbose: bool = False) -> str:
     _run([HIPCC, "-shared", "--offload-arch=gfx950", "-mcode-object-version=5", "-fPIC", "-o",
           tmp, *objs])
     os.replace(tmp, LIB)
+    tmp = SYNTH_LIB + ".tmp"
+    _run([HIPCC, "-shared", "--offload-arch=gfx950", "-mcode-object-version=5", "-fPIC", "-o",
+          tmp, os.path.join(BUILD, "synth_gen.hip.o")])
+    os.replace(tmp, SYNTH_LIB)
     return LIB
 
 

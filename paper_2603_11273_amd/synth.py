@@ -12,13 +12,17 @@ Two kinds of generator live here.
   from numpy's seeded PCG64 generator.
 * Large tensors (model parameters, synthetic encoder outputs, pre-filled
   self-attention caches) come from a counter-based integer hash so the very
-  same values can be produced on the CPU (for the oracle) and directly in
-  device memory (for the benchmark at full size) without a multi-gigabyte
-  host round trip.  The hash is Chris Wellons' "lowbias32" integer mixer
+  same values can be produced on the CPU (for the oracle, with torch integer
+  ops) and directly in device memory (for the benchmark at full size, with
+  the small HIP kernel of libasr_synth.so) without a multi-gigabyte host
+  round trip.  The hash is Chris Wellons' "lowbias32" integer mixer
   (published with his hash-prospector project); every value it yields is an
   integer multiple of a power of two with at most 8 significant bits, so it
   is exactly representable in float32 *and* bfloat16.  That makes the
-  bf16-path inputs identical on both sides with no rounding step.
+  bf16-path inputs identical on both sides with no rounding step.  The
+  "fine" variant adds a second draw 2^10 times finer (at most 18
+  significant bits: exact in float32, generally not in bfloat16), for the
+  parity cases that must see weights the bf16 path has to round.
 """
 from __future__ import annotations
 
@@ -148,17 +152,58 @@ def hash_tensor(seed: int, stream: int, start: int, count: int, device="cpu"):
     return _lowbias32_t((h + k2) & _M32)
 
 
+FINE_STREAM = 0x80000000          # stream id offset of the fine term's draws
+
+_SYNTH_LIB = None
+
+
+def _synth_lib():
+    """The device generator (libasr_synth.so, built next to this file)."""
+    global _SYNTH_LIB
+    if _SYNTH_LIB is None:
+        import ctypes as C
+        import os
+
+        import torch  # noqa: F401  (binds the library to torch's HIP runtime)
+        path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libasr_synth.so")
+        if not os.path.exists(path):
+            raise ImportError(f"{path} is missing: build it with "
+                              "`python -m paper_2603_11273_amd.build`")
+        lib = C.CDLL(path)
+        lib.asr_synth_grid.restype = C.c_int
+        lib.asr_synth_grid.argtypes = [C.c_void_p, C.c_int64, C.c_uint32, C.c_uint32, C.c_uint32,
+                                       C.c_int32, C.c_int32, C.c_float, C.c_int32, C.c_uint32,
+                                       C.c_uint32, C.c_void_p]
+        _SYNTH_LIB = lib
+    return _SYNTH_LIB
+
+
 def grid_values(seed: int, stream: int, shape, kmax: int, bits: int, device="cpu",
-                offset: float = 0.0, chunk: int = 1 << 24):
+                offset: float = 0.0, chunk: int = 1 << 24, fine: bool = False):
     """float32 tensor of (k * 2^-bits + offset), k uniform on [-kmax, kmax].
 
     kmax <= 255 keeps every k*2^-bits exactly representable in bfloat16; with
-    offset 1.0 (LayerNorm gains) the value is still exact in float32.
+    offset 1.0 (LayerNorm gains) the value is still exact in float32.  fine:
+    plus j * 2^-(bits + 10), j uniform on [-255, 255] from the stream
+    FINE_STREAM + stream (exact in float32, generally not in bfloat16).
+    CPU tensors come from torch integer ops, device tensors from the HIP
+    generator; the two agree bit for bit.
     """
     import torch
     assert 0 < kmax <= 255
     numel = int(np.prod(shape)) if len(shape) else 1
+    assert numel <= 1 << 32
     out = torch.empty(numel, dtype=torch.float32, device=device)
+    if out.device.type != "cpu":
+        k1, k2 = stream_keys(seed, stream)
+        f1, f2 = stream_keys(seed, FINE_STREAM + stream)
+        with torch.cuda.device(out.device):
+            st = torch.cuda.current_stream().cuda_stream
+            rc = _synth_lib().asr_synth_grid(out.data_ptr(), numel, 0, k1, k2, kmax, bits,
+                                             float(offset), int(fine), f1, f2, st)
+        if rc != 0:
+            raise RuntimeError(f"asr_synth_grid failed ({rc})")
+        return out.view(*shape)
     levels = 2 * kmax + 1
     scale = 2.0 ** (-bits)
     for s in range(0, numel, chunk):
@@ -168,6 +213,9 @@ def grid_values(seed: int, stream: int, shape, kmax: int, bits: int, device="cpu
         v = k.to(torch.float32) * scale
         if offset:
             v = v + offset
+        if fine:
+            j = ((hash_tensor(seed, FINE_STREAM + stream, s, n, device) * 511) >> 32) - 255
+            v = v + j.to(torch.float32) * 2.0 ** (-(bits + 10))
         out[s:s + n] = v
     return out.view(*shape)
 
@@ -218,15 +266,31 @@ def param_specs(shape: ModelShape):
     return specs
 
 
-def model_params(shape: ModelShape, seed: int, device="cpu"):
-    """Ordered dict name -> float32 tensor (values exact in bfloat16 for matrices)."""
+def model_params(shape: ModelShape, seed: int, device="cpu", fine: bool = False):
+    """Ordered dict name -> float32 tensor.  Values are exact in bfloat16,
+    unless fine (then every tensor carries the finer second draw)."""
     params = {}
     for i, (name, shp, kind) in enumerate(param_specs(shape)):
         if kind == "g":
-            params[name] = grid_values(seed, i, shp, 141, 12, device, offset=1.0)
+            params[name] = grid_values(seed, i, shp, 141, 12, device, offset=1.0, fine=fine)
         else:
-            params[name] = grid_values(seed, i, shp, 141, 12, device)
+            params[name] = grid_values(seed, i, shp, 141, 12, device, fine=fine)
     return params
+
+
+def bf16_rounded_params(params: dict) -> dict:
+    """The parameters as a bf16 context holds them: matrices (linear and conv
+    weights, the token embedding) rounded to bfloat16 (round to nearest
+    even, torch's conversion) and back to float32; vectors (biases, LayerNorm
+    gains and shifts, positional embeddings) stay float32."""
+    import torch
+    out = {}
+    for name, t in params.items():
+        if name.endswith(".w") or name == "tok_emb":
+            out[name] = t.to(torch.bfloat16).to(torch.float32)
+        else:
+            out[name] = t
+    return out
 
 
 def encoder_output(seed: int, index: int, d_model: int, device="cpu"):

@@ -30,12 +30,12 @@ def rel_err(g, o):
     return float(np.abs(g - o).max() / max(np.abs(o).max(), 1e-30))
 
 
-def make_context(shape, seed, max_slots=4, max_prefill=2, max_decode=4):
+def make_context(shape, seed, max_slots=4, max_prefill=2, max_decode=4, fine=False):
     from paper_2603_11273_amd import asr
     ctx = asr.Context(asr.model_cfg(shape, max_slots=max_slots, max_prefill=max_prefill,
                                     max_decode=max_decode), device=0)
     ctx.bind()
-    params = synth.model_params(shape, seed, device="cuda")
+    params = synth.model_params(shape, seed, device="cuda", fine=fine)
     tensors = list(params.values())
     assert len(tensors) == ctx.n_params()
     for i, t in enumerate(tensors):
@@ -46,8 +46,12 @@ def make_context(shape, seed, max_slots=4, max_prefill=2, max_decode=4):
     return ctx
 
 
-def cpu_params(shape, seed):
-    return synth.model_params(shape, seed, device="cpu")
+def cpu_params(shape, seed, fine=False, bf16_rounded=False):
+    """The oracle's parameters: the same generator on the CPU; bf16_rounded
+    gives them as a bf16 context holds them (matrices rounded to nearest
+    even)."""
+    p = synth.model_params(shape, seed, device="cpu", fine=fine)
+    return synth.bf16_rounded_params(p) if bf16_rounded else p
 
 
 def check_logits(g, o, tol, label=""):

@@ -69,20 +69,25 @@ def _check_greedy(tokens, pcm, P, shape):
     return near
 
 
-def test_serve_greedy_matches_oracle_under_preemption():
+@pytest.mark.parametrize("overlap", [False, True])
+def test_serve_greedy_matches_oracle_under_preemption(overlap):
     """Whisper-tiny shape, fp32: a burst of 6 clips of 1-2.6 s (3-7 tokens at
     2.7 tokens per audio-second), 4 slots, 2 admissions per step, cross share
     10 and a pool of 52 positions: four requests are admitted over the first
-    two steps (need 46), and their growth overflows the pool at the fourth
-    step, so requests are evicted and later recomputed.  Every request's
-    tokens must still follow the oracle."""
+    two steps (need 46), and their growth overflows the pool a few steps
+    later, so requests are evicted and later recomputed.  Every request's
+    tokens must still follow the oracle.  With overlap the admitted clips'
+    prefill runs on the second stream beside the running rows, and with two
+    admissions the encoder splits them into two clip groups on streams of
+    their own."""
     from paper_2603_11273_amd import asr
     shape = synth.SHAPES["tiny"]
     seed = 20260340
     ctx = make_context(shape, seed, max_slots=4, max_prefill=2, max_decode=4)
     P = cpu_params(shape, seed)
     clips, arr = _requests(seed, 6)
-    toks, pre = _serve(ctx, asr.SJF, clips, arr, kv_capacity=52, cross_tokens=10, max_admit=2)
+    toks, pre = _serve(ctx, asr.SJF, clips, arr, kv_capacity=52, cross_tokens=10, max_admit=2,
+                       overlap=overlap)
     assert pre > 0, "the pool was sized to force preemption"
     for i, pcm in enumerate(clips):
         assert len(toks[i]) == S.tokens_for(len(pcm), SR, 448, 27, 10)

@@ -29,9 +29,17 @@ def _context(shape, seed, **cap):
     return ctx, host
 
 
-def test_generator_is_device_independent():
-    a = synth.grid_values(20260314, 77, (1 << 20,), 141, 12, device="cuda").cpu()
-    b = synth.grid_values(20260314, 77, (1 << 20,), 141, 12, device="cpu")
+@pytest.mark.parametrize("kmax,bits,offset,fine", [(141, 12, 0.0, False), (141, 12, 1.0, False),
+                                                   (221, 7, 0.0, False), (141, 12, 0.0, True),
+                                                   (141, 12, 1.0, True)])
+def test_generator_is_device_independent(kmax, bits, offset, fine):
+    """The device generator (libasr_synth.so) and the CPU route (torch
+    integer ops) give bit-identical tensors, with and without the offset and
+    the fine second draw; the length is not a multiple of the launch grid."""
+    n = (1 << 20) + 77
+    a = synth.grid_values(20260314, 77, (n,), kmax, bits, device="cuda", offset=offset,
+                          fine=fine).cpu()
+    b = synth.grid_values(20260314, 77, (n,), kmax, bits, device="cpu", offset=offset, fine=fine)
     assert torch.equal(a, b)
 
 

@@ -63,3 +63,33 @@ def test_attention_operands_exact_and_structured(case):
         assert np.abs(first).max() < 8 and late.min() > 64
     else:
         assert s.max() < -64
+
+
+def test_fine_values_exact_in_fp32_not_in_bf16():
+    """The fine variant: the base draw plus j * 2^-22 (|j| <= 255) is a
+    multiple of 2^-22 (exact in float32), moves almost every value off the
+    bfloat16 grid, leaves the spread at ~0.02, and keeps the base draw (the
+    fine term is at most 255 * 2^-22 < 2^-13 away from it)."""
+    base = synth.grid_values(1, 2, (8192,), 141, 12)
+    v = synth.grid_values(1, 2, (8192,), 141, 12, fine=True)
+    scaled = v.double() * 2.0 ** 22
+    assert torch.equal(scaled, scaled.round())
+    off_grid = (v.to(torch.bfloat16).to(torch.float32) != v).float().mean()
+    assert off_grid > 0.95
+    assert abs(float(v.std()) - 0.02) < 0.002
+    d = (v - base).double() * 2.0 ** 22
+    assert float(d.abs().max()) <= 255 and float(d.abs().max()) > 200
+    g = synth.grid_values(1, 3, (4096,), 141, 12, offset=1.0, fine=True)
+    assert torch.equal((g.double() - 1.0) * 2.0 ** 22, ((g.double() - 1.0) * 2.0 ** 22).round())
+
+
+def test_bf16_rounded_params_round_matrices_only():
+    shape = synth.reduced_shape(synth.SHAPES["tiny"], 1, 1, vocab=64)
+    p = synth.model_params(shape, 3, fine=True)
+    r = synth.bf16_rounded_params(p)
+    for name, t in p.items():
+        if name.endswith(".w") or name == "tok_emb":
+            assert torch.equal(r[name], t.to(torch.bfloat16).to(torch.float32)), name
+            assert not torch.equal(r[name], t), name
+        else:
+            assert r[name] is t, name
