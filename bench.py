@@ -204,7 +204,7 @@ def main():
     # encoder runs its two clip groups on two streams, so per-launch times
     # would overlap; kernels are timed in the pass below).
     ctx.reset_timing()
-    ctx.set_timing((1 << asr.K_PREFILL) | (1 << asr.K_DECODE))
+    ctx.set_timing((1 << asr.K_PREFILL) | (1 << asr.K_DECODE) | (1 << asr.K_ENCODE))
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
@@ -232,13 +232,14 @@ def main():
     ms_step = wall * 1e3 / args.steps
     audio_s = P * 30.0
     enc_ms = tm["prefill"]["ms"] / args.steps
+    encode_ms = tm["encode"]["ms"] / args.steps
     dec_ms = tm["decode"]["ms"] / args.steps
     g = tb["gemm"]
     gemm_tflops = g["flops"] / (g["ms"] * 1e-3) / 1e12 if g["ms"] else 0.0
     da = tb["dattn"]
     dattn_gbs = da["bytes"] / (da["ms"] * 1e-3) / 1e9 if da["ms"] else 0.0
-    enc_flops = (tb["gemm"]["flops"] + tb["attn"]["flops"]) / nb
-    dec_bytes = (tb["dgemm"]["bytes"] + tb["dattn"]["bytes"] + tb["vocab"]["bytes"]) / nb
+    # algorithmic work of the timed steps, from the shapes alone
+    work = algorithmic_work(shape, P, D, kv_len, args.warmup, args.steps)
     kernels = {k: {"ms_per_step": v["ms"] / nb, "launches_per_step": v["launches"] / nb}
                for k, v in tb.items()}
 
@@ -259,14 +260,27 @@ def main():
                                "(self-KV U[10,400], 1500 cross positions)",
                    "prefill_clips": P, "decode_rows": D, "n_mels": 128, "d_model": 1280,
                    "layers": "32+32", "vocab": 51866, "parallelism": "none (1 GPU)"},
-        "encoder_audio_s_per_s": round(audio_s / (enc_ms * 1e-3), 1) if enc_ms else None,
+        "encoder_audio_s_per_s": round(audio_s / (encode_ms * 1e-3), 1) if encode_ms else None,
+        "prefill_audio_s_per_s": round(audio_s / (enc_ms * 1e-3), 1) if enc_ms else None,
         "decode_tokens_per_s": round(D / (dec_ms * 1e-3), 1) if dec_ms else None,
         "prefill_ms": round(enc_ms, 3),
+        "encoder_ms": round(encode_ms, 3),
+        "cross_kv_ms": round(enc_ms - encode_ms, 3),
         "decode_ms": round(dec_ms, 3),
-        "encoder_mfma_frac": round(enc_flops / (enc_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)
-        if enc_ms else None,
-        "decode_hbm_frac": round(dec_bytes / (dec_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)
+        # stem + encoder GEMMs + attention flops over the encoder's wall time
+        # (mel .. ln_post); cross K/V reported on its own
+        "encoder_mfma_frac": round(work["encoder_flops"] / (encode_ms * 1e-3) / 1e12
+                                   / PEAK_BF16_TFLOPS, 4) if encode_ms else None,
+        "cross_kv_mfma_frac": round(work["cross_kv_flops"] / ((enc_ms - encode_ms) * 1e-3)
+                                    / 1e12 / PEAK_BF16_TFLOPS, 4) if enc_ms > encode_ms else None,
+        # weights + cross K/V + self K/V at the timed steps' own positions
+        "decode_bytes_per_step": round(work["decode_bytes"]),
+        "decode_hbm_frac": round(work["decode_bytes"] / (dec_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)
         if dec_ms else None,
+        "work_note": "encoder flops " + f"{work['encoder_flops']:.4g}" + " and decode bytes from "
+                     "the model shape and the timed steps' cache lengths; the 64 clips' PCM is "
+                     "resident in HBM before the timed region (its host-to-device copy is not "
+                     "timed)",
         "queue_us_per_request": round(queue_us_per_req, 3),
         "kernels": kernels,
         "kernels_note": f"per-class breakdown and rooflines over {nb} further steps with the "
@@ -292,6 +306,32 @@ def main():
     print(json.dumps(result), flush=True)
 
 
+def algorithmic_work(shape, P, D, kv_len, warmup, steps):
+    """Algorithmic flops of the encoder and bytes of the decode step at the
+    benchmark's shape (2 flops per multiply-add; each operand read once).
+
+    Encoder (per clip): conv1 3000 x d x 3 n_mels, conv2 1500 x d x 3d; per
+    layer QKV 1500 x 3d x d, out-projection 1500 x d x d, FC1 and FC2
+    1500 x F x d; attention 4 x 1500^2 x 64 per head.  Cross K/V: 1500 x
+    (L_dec 2 d) x d per clip.  Decode step: every decoder weight matrix and the
+    token embedding (bf16), the cross K/V of all rows (1500 positions), and
+    the self K/V of each row over its length + 1 positions at the timed
+    steps (the cache grows by one position per step)."""
+    d, F, H, M = shape.d_model, shape.d_ffn, shape.n_head, shape.n_mels
+    Le, Ld, V = shape.n_enc, shape.n_dec, shape.vocab
+    T = 1500
+    stem = 2.0 * 3000 * d * 3 * M + 2.0 * T * d * 3 * d
+    layer = 2.0 * T * d * (3 * d + d + 2 * F) + 4.0 * T * T * 64 * H
+    enc = P * (stem + Le * layer)
+    xkv = P * 2.0 * T * (Ld * 2 * d) * d
+    w_bytes = 2.0 * (Ld * (3 * d * d + 3 * d * d + 2 * F * d) + V * d)
+    cross_bytes = 2.0 * D * Ld * 2 * T * d
+    keys = np.mean([np.sum(np.asarray(kv_len, np.int64) + warmup + k + 1) for k in range(steps)])
+    self_bytes = 2.0 * Ld * 2 * keys * d
+    return {"encoder_flops": enc, "cross_kv_flops": xkv,
+            "decode_bytes": w_bytes + cross_bytes + self_bytes}
+
+
 def serving_section(ctx, D, P, enc_ms, dec_ms, toks, steps_done):
     """Continuous batching at the large-v3 shape.
 
@@ -308,6 +348,7 @@ def serving_section(ctx, D, P, enc_ms, dec_ms, toks, steps_done):
     import numpy as np
     import torch
     from paper_2603_11273_amd import asr, synth
+    from paper_2603_11273_amd import serving_metrics as SM
 
     # 1. decode cost at 16 rows (positions stay below 448: the bench's slots
     #    start at <= 400 and have advanced steps_done + 3 positions)
@@ -373,10 +414,11 @@ def serving_section(ctx, D, P, enc_ms, dec_ms, toks, steps_done):
                          overlap=int(overlap))
         for i in range(n):
             ctx.submit(id0 + i, clips[i % n_burst][:int(n_s[i])], arrival_us=int(arr[i]))
-        first, fin, steps, busy = {}, {}, 0, 0.0
+        emit, steps, busy, n_fin = {}, 0, 0.0, 0
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        while len(fin) < n:
+        t_end = 0
+        while n_fin < n:
             now = int((time.perf_counter() - t0) * 1e6)
             ts = time.perf_counter()
             r = ctx.serve_step(now)
@@ -385,19 +427,29 @@ def serving_section(ctx, D, P, enc_ms, dec_ms, toks, steps_done):
             if r["decoded"]:
                 steps += 1
                 busy += te - ts
+            # every decoded row emits one token at the end of the step (no
+            # preemption here: the pool is unbounded)
             for rid in r["decoded"]:
-                first.setdefault(rid, end_us)
+                emit.setdefault(rid, []).append(end_us)
             for rid in r["finished"]:
-                fin[rid] = end_us
                 ctx.serve_tokens(rid)
+                n_fin += 1
+                t_end = end_us
             if not r["decoded"] and not r["admitted"]:
                 time.sleep(0.0002)
-        ttft = np.array([first[id0 + i] - arr[i] for i in range(n)]) * 1e-6
-        e2el = np.array([fin[id0 + i] - arr[i] for i in range(n)]) * 1e-6
-        pct = lambda v, p: round(float(np.percentile(v, p, method="inverted_cdf")), 4)  # noqa: E731
-        return {"requests": n, "rate_per_s": rate, "ttft_p50_s": pct(ttft, 50),
-                "ttft_p90_s": pct(ttft, 90), "e2el_p50_s": pct(e2el, 50),
-                "e2el_p90_s": pct(e2el, 90), "busy_steps": steps,
+        ids = [id0 + i for i in range(n)]
+        m = SM.latency_metrics(arr, [emit[i][0] for i in ids], [emit[i][-1] for i in ids],
+                               [len(emit[i]) for i in ids], [t for i in ids for t in emit[i]],
+                               t_end)
+        return {"requests": n, "rate_per_s": rate,
+                "ttft_p50_s": round(m["ttft_p50_us"] * 1e-6, 4),
+                "ttft_p90_s": round(m["ttft_p90_us"] * 1e-6, 4),
+                "e2el_p50_s": round(m["e2el_p50_us"] * 1e-6, 4),
+                "e2el_p90_s": round(m["e2el_p90_us"] * 1e-6, 4),
+                "tpot_mean_ms": round(m["tpot_mean_us"] * 1e-3, 3),
+                "itl_p50_ms": round(m["itl_p50_us"] * 1e-3, 3),
+                "itl_p90_ms": round(m["itl_p90_us"] * 1e-3, 3),
+                "busy_steps": steps,
                 "mean_busy_step_ms": round(busy * 1e3 / max(steps, 1), 3)}
 
     rt_rate = round(0.6 * gpu["req_per_s"], 1)
@@ -426,18 +478,24 @@ def serving_section(ctx, D, P, enc_ms, dec_ms, toks, steps_done):
         for i in range(n):
             q.submit(i, None, n_samples=int(n_s[i]), arrival_us=int(arr[i]))
         t0 = time.perf_counter()
-        info, t_end = q.serve_simulate(list(range(n)), want_token_times=False, **cost)
+        info, t_end = q.serve_simulate(list(range(n)), want_token_times=True, **cost)
         host_us = (time.perf_counter() - t0) * 1e6 / n
-        ttft = np.array([info[i]["first_us"] - arr[i] for i in range(n)]) * 1e-6
-        e2el = np.array([info[i]["finish_us"] - arr[i] for i in range(n)]) * 1e-6
-        pct = lambda v, p: float(np.percentile(v, p, method="inverted_cdf"))  # noqa: E731
+        m = SM.latency_metrics(arr, [info[i]["first_us"] for i in range(n)],
+                               [info[i]["finish_us"] for i in range(n)],
+                               [info[i]["n_tokens"] for i in range(n)],
+                               [t for i in range(n) for t in info[i]["token_us"]], t_end)
         extra = {}
         if policy == DYNAMIC:
             st = q.serve_stats()
             extra["steps_fcfs_sjf_hrrn"] = st
-        return {**extra, "ttft_p50_s": round(pct(ttft, 50), 3), "ttft_p90_s": round(pct(ttft, 90), 3),
-                "e2el_p50_s": round(pct(e2el, 50), 3), "e2el_p90_s": round(pct(e2el, 90), 3),
-                "req_per_s": round(n / ((t_end - int(arr.min())) * 1e-6), 2),
+        return {**extra, "ttft_p50_s": round(m["ttft_p50_us"] * 1e-6, 3),
+                "ttft_p90_s": round(m["ttft_p90_us"] * 1e-6, 3),
+                "e2el_p50_s": round(m["e2el_p50_us"] * 1e-6, 3),
+                "e2el_p90_s": round(m["e2el_p90_us"] * 1e-6, 3),
+                "tpot_mean_ms": round(m["tpot_mean_us"] * 1e-3, 3),
+                "itl_p50_ms": round(m["itl_p50_us"] * 1e-3, 3),
+                "itl_p90_ms": round(m["itl_p90_us"] * 1e-3, 3),
+                "req_per_s": round(m["req_per_s"], 2), "tok_per_s": round(m["tok_per_s"], 1),
                 "sched_host_us_per_request": round(host_us, 2)}
 
     names = {asr.FCFS: "fcfs", asr.SJF: "sjf", asr.HRRN: "hrrn", DYNAMIC: "dynamic"}
@@ -455,7 +513,8 @@ def serving_section(ctx, D, P, enc_ms, dec_ms, toks, steps_done):
         for pol in ("sjf", "hrrn", "dynamic"):
             case[pol]["vs_fcfs_pct"] = {
                 k: round(100.0 * (case[pol][k] - base[k]) / base[k], 1) if base[k] else None
-                for k in ("ttft_p50_s", "ttft_p90_s", "e2el_p50_s", "e2el_p90_s")}
+                for k in ("ttft_p50_s", "ttft_p90_s", "e2el_p50_s", "e2el_p90_s",
+                          "tpot_mean_ms", "itl_p50_ms", "itl_p90_ms")}
     return {"cost_model_us": cost, "decode_16_rows_ms": round(dec16_ms, 3), "gpu_burst": gpu,
             "gpu_realtime_poisson": rt,
             "simulation": sim,

@@ -27,9 +27,12 @@
  *   - Host buffers belong to the caller.  Device memory is ONE caller-provided
  *     block (asr_bind) that the library sub-allocates and never frees; the
  *     library itself never allocates device memory.
- *   - All GPU work is enqueued on the stream given to asr_bind.  asr_step and
- *     the debug readers synchronise that stream only to copy results to the
- *     host.
+ *   - GPU work is enqueued on the stream given to asr_bind.  A prefill may
+ *     fork onto streams the context owns (default priority): its clip groups
+ *     (asr_set_encoder_streams) and, with overlapped prefill, the whole
+ *     prefill; every fork waits on an event of the bound stream and is joined
+ *     back into it (or synchronised) before the call returns.  asr_step and
+ *     the debug readers synchronise only to copy results to the host.
  *   - A context is not thread-safe; calls on one context must be serialised.
  */
 #ifndef ASR_H
@@ -196,7 +199,9 @@ typedef enum {
   ASR_K_OTHER = 7,
   ASR_K_PREFILL = 8,    /* whole prefill phase of asr_step (mel .. cross K/V) */
   ASR_K_DECODE = 9,     /* whole decode phase of asr_step (embed .. argmax) */
-  ASR_K_COUNT = 10
+  ASR_K_ENCODE = 10,    /* encoder part of a prefill (mel .. ln_post, without cross K/V):
+                           from its start to the last clip group's ln_post */
+  ASR_K_COUNT = 11
 } asr_kernel_class;
 
 /* ---------------------------------------------------------------------------
@@ -309,6 +314,15 @@ asr_status asr_serve_simulate(asr_ctx* ctx, const asr_sim_cost* cost, int64_t t0
  * one chain, where every launch owns the GPU (what per-kernel timing needs).
  * Results do not depend on n. */
 asr_status asr_set_encoder_streams(asr_ctx* ctx, int32_t n);
+
+/* Decode steps replayed from HIP graphs (on = 1, the default) or launched
+ * kernel by kernel (on = 0).  With graphs, the decode kernels of each shape
+ * (row count, logits wanted) are captured once -- at that shape's second
+ * step, on a stream the context owns -- and every later step of the shape
+ * replays them on the bound stream after uploading its rows.  Results are
+ * the same either way; steps with per-launch timing selected always launch
+ * directly. */
+asr_status asr_set_decode_graphs(asr_ctx* ctx, int32_t on);
 
 /* classes is a bit mask over the asr_kernel_class values: bit k selects class
  * k, 0 turns timing off, ASR_TIME_ALL times every class.  An event pair is

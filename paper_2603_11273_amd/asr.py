@@ -18,20 +18,23 @@ ASR_OK, ASR_EINVAL, ASR_ENOMEM, ASR_EFULL, ASR_ENOTFOUND, ASR_ESTATE, ASR_ENODEV
 STATUS_NAMES = ["OK", "EINVAL", "ENOMEM", "EFULL", "ENOTFOUND", "ESTATE", "ENODEV", "EDEVICE"]
 FCFS, SJF, HRRN = 0, 1, 2
 F32, BF16 = 0, 1
-K_MEL, K_GEMM, K_ATTN, K_LN, K_DGEMM, K_DATTN, K_VOCAB, K_OTHER, K_PREFILL, K_DECODE = range(10)
+(K_MEL, K_GEMM, K_ATTN, K_LN, K_DGEMM, K_DATTN, K_VOCAB, K_OTHER, K_PREFILL, K_DECODE,
+ K_ENCODE) = range(11)
 KERNEL_CLASSES = ["mel", "gemm", "attn", "ln", "dgemm", "dattn", "vocab", "other", "prefill",
-                  "decode"]
+                  "decode", "encode"]
 TIME_ALL = (1 << len(KERNEL_CLASSES)) - 1
 
 EXPORTED = [
     "asr_create", "asr_destroy", "asr_last_error", "asr_workspace_size", "asr_bind",
     "asr_n_params", "asr_param_numel", "asr_load_weights", "asr_set_policy", "asr_submit",
     "asr_rank", "asr_pop_batch", "asr_queue_len", "asr_step", "asr_release_slot",
-    "asr_slot_info", "asr_set_encoder_streams", "asr_set_timing", "asr_get_timing",
+    "asr_slot_info", "asr_set_encoder_streams", "asr_set_decode_graphs", "asr_set_timing",
+    "asr_get_timing",
     "asr_reset_timing",
     "asr_debug_logmel", "asr_debug_encode", "asr_debug_attention", "asr_debug_set_encoder_out",
     "asr_debug_get_kv",
-    "asr_debug_set_self_kv", "asr_serve_config", "asr_serve_step", "asr_serve_plan",
+    "asr_debug_set_self_kv", "asr_serve_config", "asr_serve_step",
+    "asr_serve_plan",
     "asr_serve_tokens", "asr_serve_simulate", "asr_serve_stats",
 ]
 
@@ -112,6 +115,7 @@ def _load():
         "asr_release_slot": [vp, i32],
         "asr_slot_info": [vp, i32, P(i32), P(i64), P(i32), P(i32)],
         "asr_set_encoder_streams": [vp, i32],
+        "asr_set_decode_graphs": [vp, i32],
         "asr_set_timing": [vp, i32],
         "asr_get_timing": [vp, i32, P(C.c_double), P(i64), P(C.c_double), P(C.c_double)],
         "asr_reset_timing": [vp],
@@ -376,6 +380,10 @@ class Context:
         _check(lib.asr_set_encoder_streams(self.h, int(n)))
 
     # -- timing ---------------------------------------------------------------
+    def set_decode_graphs(self, on: bool):
+        """Replay decode steps from HIP graphs (default) or launch directly."""
+        _check(lib.asr_set_decode_graphs(self.h, int(bool(on))))
+
     def set_timing(self, classes=True):
         """True times every kernel class, False none; an int is a bit mask
         over the class numbers (K_MEL .. K_DECODE)."""

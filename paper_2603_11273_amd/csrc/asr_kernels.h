@@ -74,13 +74,16 @@ void gemm_f32(const AView& a, const float* w, int M, int N, int K, const Epilogu
 // Number of CUs the persistent bf16 GEMM leaves free (process-wide; 0 = none).
 void gemm_set_cu_reserve(int n);
 
-// Skinny GEMM for decode rows: partial[s][b][n] = sum_{k in split s} x[b][k] w[n][k].
-// Returns the number of K-splits used (the partial buffer holds splits*D*N floats).
-int dgemm_bf16(const bf16_t* x, const bf16_t* w, int D, int N, int K, float* partial,
-               int max_splits, hipStream_t s);
-int dgemm_splits(int K);   // K-slices dgemm_bf16 uses (K / 128)
-int dgemm_f32(const float* x, const float* w, int D, int N, int K, float* partial,
-              int max_splits, hipStream_t s);
+// Skinny GEMM for decode rows (D <= 128, N % 32 == 0, K % 64 == 0), x [D][K]
+// times w [N][K]^T.  DG_PARTIAL: out = float32 partial sums over K slices,
+// partial[s][b][n] for s < dgemm_splits(N, K) (returned); DG_BIAS / DG_GELU:
+// out[b][n] = (gelu)(sum + bias[n]) in bf16 (returns 1).
+enum DgEpi : int32_t { DG_PARTIAL = 0, DG_BIAS = 1, DG_GELU = 2 };
+int dgemm_bf16(const bf16_t* x, const bf16_t* w, int D, int N, int K, int epi,
+               const float* bias, void* out, hipStream_t s);
+int dgemm_splits(int N, int K);
+// fp32 path: out[b][n] = sum_k x[b][k] w[n][k] (one partial slice, no bias).
+void dgemm_f32(const float* x, const float* w, int D, int N, int K, float* out, hipStream_t s);
 // out = epilogue(sum_s partial[s] + bias): mode 0 store (T), 1 gelu (T), 2 residual add (f32).
 template <typename T>
 void dgemm_reduce(const float* partial, int splits, int D, int N, const float* bias, int mode,
@@ -131,14 +134,19 @@ void flash_attn_f32(const float* qkv, float* out, int B, int n_head, hipStream_t
 constexpr int DA_NCH = 4;    // chunks per row at most (1500 cross keys / 384)
 constexpr int DA_REC = 66;   // floats per partial: max, sum, 64 weighted values
 int decode_attn_part_floats(int D, int n_head);
+// Self: fp32 contexts read q, k, v from the fused QKV output qkv [D][3d];
+// bf16 contexts from the float32 partial sums of the QKV product plus its
+// bias (qkv_part[s][b][3d], s < qkv_splits).
 template <typename T>
-void decode_self_attn(const T* qkv, T* cache, int64_t slot_stride, int64_t layer_off,
-                      const int32_t* slots, const int32_t* pos, int D, int n_head, T* out,
-                      float* part, hipStream_t s);
+void decode_self_attn(const T* qkv, const float* qkv_part, int qkv_splits, const float* qkv_bias,
+                      T* cache, int64_t slot_stride, int64_t layer_off, const int32_t* slots,
+                      const int32_t* pos, int D, int n_head, T* out, float* part, hipStream_t s);
+// The cross attention takes its queries as the float32 partial sums of the
+// query product: q[b] = bias + sum_{s < q_splits} q_part[s][b].
 template <typename T>
-void decode_cross_attn(const T* q, T* cache, int64_t slot_stride, int64_t layer_off,
-                       const int32_t* slots, int D, int n_head, T* out, float* part,
-                       hipStream_t s);
+void decode_cross_attn(const float* q_part, int q_splits, const float* q_bias, T* cache,
+                       int64_t slot_stride, int64_t layer_off, const int32_t* slots, int D,
+                       int n_head, T* out, float* part, hipStream_t s);
 
 template <typename T>
 void embed(const T* tok_emb, const float* pos_emb, const int32_t* tokens, const int32_t* pos,
@@ -154,6 +162,15 @@ struct MelTables {
 };
 void log_mel(const float* const* pcm_ptrs, const int64_t* n_samples, int n_clips, int n_mels,
              const MelTables& t, float* mel_raw, uint32_t* clip_max, hipStream_t s);
+// The same with the clips' pointers and lengths in the kernel arguments (no
+// device-side lists), for up to kMelArgClips clips.
+constexpr int kMelArgClips = 64;
+struct MelClipArgs {
+  const float* ptr[kMelArgClips];
+  int64_t n[kMelArgClips];
+};
+void log_mel_args(const MelClipArgs& clips, int n_clips, int n_mels, const MelTables& t,
+                  float* mel_raw, uint32_t* clip_max, hipStream_t s);
 template <typename T>
 void mel_normalize(const float* mel_raw, const uint32_t* clip_max, int n_clips, int n_mels,
                    T* out, int pad_rows, hipStream_t s);

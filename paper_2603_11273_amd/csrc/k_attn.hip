@@ -381,8 +381,14 @@ __device__ __forceinline__ void load8(const bf16_t* p, float* v) {
 // the chunks' (max, sum, weighted values).
 constexpr int DA_CK = 384;
 
+// SELF: queries, keys and values of the step come from the fused QKV output
+// `src` [D][3d].  Cross: the query is bias + the q_splits float32 partial
+// sums of the query product (q_part[s][row][d]).
 template <typename T, bool SELF>
-__global__ __launch_bounds__(256) void k_decode_attn(const T* __restrict__ src, T* cache,
+__global__ __launch_bounds__(256) void k_decode_attn(const T* __restrict__ src,
+                                                     const float* __restrict__ q_part,
+                                                     int q_splits, const float* __restrict__ q_bias,
+                                                     int D, T* cache,
                                                      int64_t slot_stride, int64_t layer_off,
                                                      const int32_t* slots, const int32_t* pos,
                                                      int n_head, float* __restrict__ part) {
@@ -394,7 +400,7 @@ __global__ __launch_bounds__(256) void k_decode_attn(const T* __restrict__ src, 
   const int h = blockIdx.x, row = blockIdx.y, chunk = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int d = n_head * 64;
-  const int ldsrc = SELF ? 3 * d : d;
+  const int ldsrc = 3 * d;
   const int n = SELF ? pos[row] + 1 : kCtx;
   const int k0 = chunk * DA_CK;
   if (k0 >= n) return;                          // this row has fewer chunks (uniform per block)
@@ -402,9 +408,18 @@ __global__ __launch_bounds__(256) void k_decode_attn(const T* __restrict__ src, 
   const int slot = slots[row];
   T* kb = cache + (int64_t)slot * slot_stride + layer_off + (int64_t)h * CTX * 64;
   T* vb = kb + (int64_t)n_head * CTX * 64;
-  const T* srow = src + (int64_t)row * ldsrc + h * 64;
+  const T* srow = SELF ? src + (int64_t)row * ldsrc + h * 64 : nullptr;
 
-  if (tid < 64) qs[tid] = St<T>::ld(srow, tid) * 0.125f;
+  if (tid < 64) {
+    if constexpr (SELF) {
+      qs[tid] = St<T>::ld(srow, tid) * 0.125f;
+    } else {
+      const int c = h * 64 + tid;
+      float v = q_bias[c];
+      for (int sp = 0; sp < q_splits; ++sp) v += q_part[((int64_t)sp * D + row) * d + c];
+      qs[tid] = v * 0.125f;
+    }
+  }
   if (SELF && tid < 128 && n - 1 >= k0 && n - 1 < k0 + kn) {
     // the chunk holding position n-1 stores this step's k, v there
     int j = tid & 63;
@@ -528,35 +543,203 @@ __global__ __launch_bounds__(256) void k_decode_combine(const float* __restrict_
   St<T>::st(out, (int64_t)row * n_head * 64 + h * 64 + lane, num / den);
 }
 
+// bf16 decode attention with every K and V row of the block's keys in
+// flight at once: each thread issues the 16-byte loads of its share of all
+// keys (8 lanes per key, 32 keys per pass, NP passes) for K and V before any
+// arithmetic, so the value stream's latency hides behind the scores and the
+// softmax; scores stay in registers (one cross-lane reduction per key), and
+// three block barriers remain.  The query (and, SELF, this step's key and
+// value) is the bias plus the qp_splits float32 partial sums of its product
+// (qp[s][row][...]).  SELF: one block per (row, head) over all position + 1
+// keys, writing the output directly; the new key and value, rounded to bf16,
+// go into the cache at the last position and into the scores from LDS.
+// Cross: one block per (row, head, 384-key chunk), leaving a (max, sum,
+// weighted values) record for the combine kernel.
+template <bool SELF, int NP>
+__global__ __launch_bounds__(256) void k_dattn_bf16(const float* __restrict__ qp, int qp_splits,
+                                                    const float* __restrict__ qp_bias, int D,
+                                                    bf16_t* cache, int64_t slot_stride,
+                                                    int64_t layer_off, const int32_t* slots,
+                                                    const int32_t* pos, int n_head,
+                                                    float* __restrict__ part,
+                                                    bf16_t* __restrict__ out) {
+  constexpr int CTX = SELF ? kTextCtx : kCtx;
+  constexpr int CK = NP * 32;                       // keys per block
+  __shared__ float qs[64];
+  __shared__ __attribute__((aligned(16))) bf16_t kvnew[2][64];
+  __shared__ float red[2][4];
+  __shared__ float ored[4][64];
+  const int h = blockIdx.x, row = blockIdx.y, chunk = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int d = n_head * 64;
+  const int n = SELF ? pos[row] + 1 : kCtx;
+  const int k0 = chunk * CK;
+  if (k0 >= n) return;
+  const int kn = min(CK, n - k0);
+  const int slot = slots[row];
+  bf16_t* kb = cache + (int64_t)slot * slot_stride + layer_off + (int64_t)h * CTX * 64;
+  bf16_t* vb = kb + (int64_t)n_head * CTX * 64;
+  const int sub = lane >> 3, dc = (lane & 7) * 8;
+  const int ld = SELF ? 3 * d : d;                  // row stride of the partial sums
+
+  // all loads of the block's cached keys first (SELF: the last key is new)
+  const int kcache = SELF ? kn - 1 : kn;
+  uint4 kr[NP], vr[NP];
+  const uint4 zero = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const int kk = p * 32 + wave * 8 + sub, key = k0 + kk;
+    kr[p] = zero;
+    vr[p] = zero;
+    if (kk < kcache) {
+      kr[p] = *(const uint4*)(kb + (int64_t)key * 64 + dc);
+      vr[p] = *(const uint4*)(vb + (int64_t)key * 64 + dc);
+    }
+  }
+  // query (and, SELF, the new key and value): bias + the product's partials
+  if (tid < (SELF ? 192 : 64)) {
+    const int part_i = tid >> 6, j = tid & 63;       // 0: q, 1: k, 2: v
+    const int c = part_i * d + h * 64 + j;
+    float v = qp_bias[c];
+    for (int sp = 0; sp < qp_splits; ++sp) v += qp[((int64_t)sp * D + row) * ld + c];
+    if (part_i == 0) {
+      qs[j] = v * 0.125f;
+    } else {
+      const bf16_t b = f2bf(v);
+      kvnew[part_i - 1][j] = b;
+      (part_i == 1 ? kb : vb)[(int64_t)(n - 1) * 64 + j] = b;
+    }
+  }
+  __syncthreads();
+  if (SELF) {
+#pragma unroll
+    for (int p = 0; p < NP; ++p)
+      if (p * 32 + wave * 8 + sub == kn - 1) {
+        kr[p] = *(const uint4*)&kvnew[0][dc];
+        vr[p] = *(const uint4*)&kvnew[1][dc];
+      }
+  }
+  float qv[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) qv[i] = qs[dc + i];
+
+  // scores: 8 dims per lane, summed over the key's 8 lanes
+  float sc[NP];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    float kv[8];
+    load8((const bf16_t*)&kr[p], kv);
+    float a = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) a = fmaf(qv[i], kv[i], a);
+    a += __shfl_xor(a, 1, 64);
+    a += __shfl_xor(a, 2, 64);
+    a += __shfl_xor(a, 4, 64);
+    const int kk = p * 32 + wave * 8 + sub;
+    sc[p] = kk < kn ? a : -INFINITY;
+    mx = fmaxf(mx, sc[p]);
+  }
+  mx = wave_max(mx);
+  if (lane == 0) red[0][wave] = mx;
+  __syncthreads();
+  const float M = fmaxf(fmaxf(red[0][0], red[0][1]), fmaxf(red[0][2], red[0][3]));
+
+  // probabilities and the weighted value sum
+  float l = 0.f, acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const float pr = expf(sc[p] - M);                // 0 for keys past the chunk
+    l += pr;
+    float vv[8];
+    load8((const bf16_t*)&vr[p], vv);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = fmaf(pr, vv[i], acc[i]);
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    float a = acc[i];
+    a += __shfl_xor(a, 8, 64);
+    a += __shfl_xor(a, 16, 64);
+    a += __shfl_xor(a, 32, 64);
+    acc[i] = a;
+  }
+  // each key's probability was added by its 8 lanes
+  l = wave_sum(l) * 0.125f;
+  if (lane < 8) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ored[wave][dc + i] = acc[i];
+  }
+  if (lane == 0) red[1][wave] = l;
+  __syncthreads();
+  if (tid < 64) {
+    const float o = ored[0][tid] + ored[1][tid] + ored[2][tid] + ored[3][tid];
+    const float L = red[1][0] + red[1][1] + red[1][2] + red[1][3];
+    if constexpr (SELF) {
+      out[(int64_t)row * d + h * 64 + tid] = f2bf(o / L);
+    } else {
+      float* rec = part + (((int64_t)row * n_head + h) * DA_NCH + chunk) * DA_REC;
+      rec[2 + tid] = o;
+      if (tid == 0) {
+        rec[0] = M;
+        rec[1] = L;
+      }
+    }
+  }
+}
+
 int decode_attn_part_floats(int D, int n_head) { return D * n_head * DA_NCH * DA_REC; }
 
 template <typename T>
-void decode_self_attn(const T* qkv, T* cache, int64_t slot_stride, int64_t layer_off,
-                      const int32_t* slots, const int32_t* pos, int D, int n_head, T* out,
-                      float* part, hipStream_t s) {
+void decode_self_attn(const T* qkv, const float* qkv_part, int qkv_splits, const float* qkv_bias,
+                      T* cache, int64_t slot_stride, int64_t layer_off, const int32_t* slots,
+                      const int32_t* pos, int D, int n_head, T* out, float* part,
+                      hipStream_t s) {
   if (D <= 0) return;
+  if constexpr (sizeof(T) == 2) {
+    static_assert(kTextCtx % 32 == 0, "passes");
+    k_dattn_bf16<true, kTextCtx / 32><<<dim3(n_head, D, 1), 256, 0, s>>>(
+        qkv_part, qkv_splits, qkv_bias, D, (bf16_t*)cache, slot_stride, layer_off, slots, pos,
+        n_head, part, (bf16_t*)out);
+    return;
+  }
   constexpr int nch = (kTextCtx + DA_CK - 1) / DA_CK;
-  k_decode_attn<T, true><<<dim3(n_head, D, nch), 256, 0, s>>>(qkv, cache, slot_stride, layer_off,
-                                                              slots, pos, n_head, part);
+  k_decode_attn<T, true><<<dim3(n_head, D, nch), 256, 0, s>>>(
+      qkv, nullptr, 0, nullptr, D, cache, slot_stride, layer_off, slots, pos, n_head, part);
   k_decode_combine<T, true><<<(D * n_head + 3) / 4, 256, 0, s>>>(part, pos, D, n_head, out);
 }
 template <typename T>
-void decode_cross_attn(const T* q, T* cache, int64_t slot_stride, int64_t layer_off,
-                       const int32_t* slots, int D, int n_head, T* out, float* part,
-                       hipStream_t s) {
+void decode_cross_attn(const float* q_part, int q_splits, const float* q_bias, T* cache,
+                       int64_t slot_stride, int64_t layer_off, const int32_t* slots, int D,
+                       int n_head, T* out, float* part, hipStream_t s) {
   if (D <= 0) return;
   constexpr int nch = (kCtx + DA_CK - 1) / DA_CK;
-  k_decode_attn<T, false><<<dim3(n_head, D, nch), 256, 0, s>>>(q, cache, slot_stride, layer_off,
-                                                               slots, nullptr, n_head, part);
+  if constexpr (sizeof(T) == 2) {
+    static_assert(DA_CK % 32 == 0, "passes");
+    k_dattn_bf16<false, DA_CK / 32><<<dim3(n_head, D, nch), 256, 0, s>>>(
+        q_part, q_splits, q_bias, D, (bf16_t*)cache, slot_stride, layer_off, slots, nullptr,
+        n_head, part, nullptr);
+    k_decode_combine<T, false><<<(D * n_head + 3) / 4, 256, 0, s>>>(part, nullptr, D, n_head, out);
+    return;
+  }
+  k_decode_attn<T, false><<<dim3(n_head, D, nch), 256, 0, s>>>(
+      nullptr, q_part, q_splits, q_bias, D, cache, slot_stride, layer_off, slots, nullptr, n_head,
+      part);
   k_decode_combine<T, false><<<(D * n_head + 3) / 4, 256, 0, s>>>(part, nullptr, D, n_head, out);
 }
-template void decode_self_attn<float>(const float*, float*, int64_t, int64_t, const int32_t*,
-                                      const int32_t*, int, int, float*, float*, hipStream_t);
-template void decode_self_attn<bf16_t>(const bf16_t*, bf16_t*, int64_t, int64_t, const int32_t*,
-                                       const int32_t*, int, int, bf16_t*, float*, hipStream_t);
-template void decode_cross_attn<float>(const float*, float*, int64_t, int64_t, const int32_t*,
-                                       int, int, float*, float*, hipStream_t);
-template void decode_cross_attn<bf16_t>(const bf16_t*, bf16_t*, int64_t, int64_t,
-                                        const int32_t*, int, int, bf16_t*, float*, hipStream_t);
+template void decode_self_attn<float>(const float*, const float*, int, const float*, float*,
+                                      int64_t, int64_t, const int32_t*, const int32_t*, int, int,
+                                      float*, float*, hipStream_t);
+template void decode_self_attn<bf16_t>(const bf16_t*, const float*, int, const float*, bf16_t*,
+                                       int64_t, int64_t, const int32_t*, const int32_t*, int, int,
+                                       bf16_t*, float*, hipStream_t);
+template void decode_cross_attn<float>(const float*, int, const float*, float*, int64_t,
+                                       int64_t, const int32_t*, int, int, float*, float*,
+                                       hipStream_t);
+template void decode_cross_attn<bf16_t>(const float*, int, const float*, bf16_t*, int64_t,
+                                        int64_t, const int32_t*, int, int, bf16_t*, float*,
+                                        hipStream_t);
 
 }  // namespace asr

@@ -5,9 +5,9 @@
 //    (bias, exact GELU, fp32 residual add, conv-stem row mapping, scatter of
 //    all decoder layers' cross K/V into a slot's cache).
 //  * gemm_f32: the same contract in plain fp32 FMA (the fp32 model path).
-//  * dgemm_bf16 / dgemm_f32: skinny products for the decode rows with K split
-//    across workgroups (weights streamed once), then a reduce kernel that
-//    applies the epilogue.
+//  * dgemm_bf16 / dgemm_f32: skinny products for the decode rows (weights
+//    streamed once): bias / GELU fused into one slice, or float32 partial
+//    sums of a few K slices that the next kernel adds up.
 //  * vocab_argmax_bf16: the tied vocabulary projection fused with a per-row
 //    argmax (lowest index on ties) over each 64-column tile, finished by a
 //    deterministic cross-tile reduction.
@@ -389,9 +389,7 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(AView a, const bf16_t
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
-#ifndef ASR_GEMM_CEILING_PROBE
     if (kt + 1 < nk) GEMM_GLOAD(ra, rb, (kt + 1) * BK);
-#endif
     const bf16_t* Ac = a_frag + cur * BM * BK;
     const bf16_t* Bc = b_frag + cur * BN * BK;
     bf16x8 af[2][FM], bfr[2][FN];
@@ -418,9 +416,7 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(AView a, const bf16_t
         for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[p][i], bfr[p][j], acc[i][j], 0, 0, 0);
     }
-#ifndef ASR_GEMM_CEILING_PROBE
     if (kt + 1 < nk) GEMM_SSTORE(ra, rb, cur ^ 1);
-#endif
     __syncthreads();
   }
 #undef GEMM_GLOAD
@@ -1404,102 +1400,218 @@ void gemm_f32(const AView& a, const float* w, int M, int N, int K, const Epilogu
 }
 
 // ---------------------------------------------------------------------------
-// Decode GEMMs
+// Decode GEMMs and the vocabulary projection (skinny products)
 // ---------------------------------------------------------------------------
-// One block: 128 output columns (one wave per 32) x all decode rows (up to
-// 128) over one 128-deep K slice.  Every global load of the block is issued
-// up front: the activation slice [128][128] goes to LDS (shared by the four
-// waves), each wave's 32 weight rows x 128 go straight to registers in MFMA
-// operand layout.  The weight rows are the MFMA "A" operand and are read from
-// memory exactly once; partial sums of each K slice go to `partial`.
-constexpr int DG_KC = 128;
+// A decode step multiplies at most 128 rows by each weight matrix once, so
+// the product streams the weights from HBM (128 flops per weight byte, far
+// below the MFMA ridge) and the rows ride along from L2.  A block owns a
+// strip of 32 WN weight rows (output columns) and all 128 row slots over a K
+// range, in 64-deep chunks: each chunk's weight tile and activation tile go
+// global -> LDS with global_load_lds_dwordx4, eight lanes per 128-byte row
+// segment (whole cache lines per instruction), into an NS-stage ring with the
+// round-robin XOR swizzle of the encoder GEMM (16-byte slot c of row r holds
+// chunk c ^ ((r >> 1) & 7): conflict-free fragment reads).  Wave w computes
+// strip w % WN against 32 WN activation rows with v_mfma_f32_32x32x16_bf16:
+// weight rows are the "A" operand, activation rows the "B" operand.
+constexpr int SK_BK = 64;          // K per chunk
 
-__global__ __launch_bounds__(256) void k_dgemm_bf16(const bf16_t* __restrict__ x,
-                                                    const bf16_t* __restrict__ w, int D, int N,
-                                                    int K, float* partial) {
-  __shared__ __attribute__((aligned(16))) bf16_t Xs[128 * DG_KC];   // [row][k], swizzled chunks
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int n0 = blockIdx.x * 128 + wave * 32, split = blockIdx.y;
-  const int k0 = split * DG_KC;
+__device__ __forceinline__ int sk_swz(int row) { return (row >> 1) & 7; }
+
+enum SkEpi : int32_t { SK_PARTIAL = 0, SK_BIAS = 1, SK_GELU = 2, SK_ARGMAX = 3 };
+
+// Larger key = larger value, then lower index.  Any NaN gets the largest
+// value key so that it always wins and the finishing pass reports it.
+__device__ __forceinline__ uint64_t argmax_key(float v, int n) {
+  uint32_t o = (v != v) ? 0xffffffffu : ordered_u32(v);
+  return ((uint64_t)o << 32) | (uint64_t)(0xffffffffu - (uint32_t)n);
+}
+
+struct SkOut {
+  void* out;            // PARTIAL: float [splits][D][N]; BIAS/GELU: bf16 [D][N]
+  const float* bias;    // BIAS/GELU
+  uint64_t* keys;       // ARGMAX: [D][N / 32] best key per 32-row tile
+  float* logits;        // ARGMAX: optional float [D][N]
+};
+
+template <int WN, int NS, int EPI>
+__global__ __launch_bounds__(256) void k_skinny_bf16(const bf16_t* __restrict__ x,
+                                                     const bf16_t* __restrict__ w, int D, int N,
+                                                     int K, int KC, SkOut o) {
+  constexpr int RB = WN;                         // row blocks of 32 per wave
+  constexpr int WR = 32 * WN;                    // weight rows per block
+  constexpr int STAGE = (WR + 128) * SK_BK;      // elements per ring stage
+  constexpr int LPC = 4 + WN;                    // DMA instructions per wave per chunk
+  extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int l32 = lane & 31, lh = lane >> 5;
-  // activation slice: 128 rows x 16 chunks of 16 bytes, 8 chunks per thread
-  uint4 xr[8];
+  const int n0 = blockIdx.x * WR, split = blockIdx.y;
+  const int kb = split * KC, nck = KC / SK_BK;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) bf16_t*)smem);
+  // DMA: instruction i of a wave fills rows 8 i .. 8 i + 7 of its share; lane
+  // l lands at slot l % 8 of row l / 8 and fetches chunk (l % 8) ^ swz(row)
+  uint32_t xdst[4], wdst[WN], xoff[4], woff[WN];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int c = tid + i * 256, row = c >> 4, ch = c & 15;
-    xr[i] = *(const uint4*)(x + (int64_t)min(row, D - 1) * K + k0 + ch * 8);
+  for (int i = 0; i < 4; ++i) {
+    const int row = wave * 32 + i * 8;                               // activation rows
+    xdst[i] = __builtin_amdgcn_readfirstlane(lds0 + (uint32_t)((WR + row) * SK_BK * 2));
+    const int r = row + (lane >> 3);
+    xoff[i] = (uint32_t)(((int64_t)min(r, D - 1) * K + kb + (((lane & 7) ^ sk_swz(r)) * 8)) * 2);
   }
-  // weight fragments: row n0 + lane%32, k = k0 + 16 s + 8 (lane/32)
-  bf16x8 wf[DG_KC / 16];
-  const bf16_t* wp = w + (int64_t)min(n0 + l32, N - 1) * K + k0 + lh * 8;
 #pragma unroll
-  for (int s2 = 0; s2 < DG_KC / 16; ++s2) wf[s2] = *(const bf16x8*)(wp + s2 * 16);
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int c = tid + i * 256, row = c >> 4, ch = c & 15;
-    *(uint4*)&Xs[row * DG_KC + ((ch ^ (row & 15)) * 8)] = xr[i];
+  for (int i = 0; i < WN; ++i) {
+    const int row = wave * 8 * WN + i * 8;                           // weight rows
+    wdst[i] = __builtin_amdgcn_readfirstlane(lds0 + (uint32_t)(row * SK_BK * 2));
+    const int r = row + (lane >> 3);
+    woff[i] = (uint32_t)(((int64_t)min(n0 + r, N - 1) * K + kb + (((lane & 7) ^ sk_swz(r)) * 8)) * 2);
   }
-  __syncthreads();
-  if (n0 >= N) return;
-  const int nb = (D + 31) / 32;
-  f32x16 acc[4];
+  auto issue = [&](int c) {
+    const uint32_t so = (uint32_t)((c % NS) * STAGE * 2);
+    const bf16_t* xk = x + c * SK_BK;
+    const bf16_t* wk = w + c * SK_BK;
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
+    for (int i = 0; i < 4; ++i) lds_dma16_s(xdst[i] + so, xoff[i], xk);
+#pragma unroll
+    for (int i = 0; i < WN; ++i) lds_dma16_s(wdst[i] + so, woff[i], wk);
+  };
+  const int strip = wave % WN, rg = wave / WN;                      // this wave's strip, row group
+  const int wrow = strip * 32 + l32, sww = sk_swz(wrow);
+  int xrow[RB], swx[RB];
+#pragma unroll
+  for (int j = 0; j < RB; ++j) {
+    xrow[j] = (rg * RB + j) * 32 + l32;
+    swx[j] = sk_swz(xrow[j]);
+  }
+  f32x16 acc[RB];
+#pragma unroll
+  for (int j = 0; j < RB; ++j)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
+
 #pragma unroll
-  for (int s2 = 0; s2 < DG_KC / 16; ++s2) {
-    const int ch = s2 * 2 + lh;
+  for (int c = 0; c < NS - 1; ++c)
+    if (c < nck) issue(c);
+  for (int c = 0; c < nck; ++c) {
+    // this wave's loads of chunk c are done when at most the later issued
+    // chunks' loads are outstanding; the barrier then publishes every wave's
+    // share and frees the stage of chunk c - 1 for chunk c + NS - 1
+    wait_vmcnt_rt<LPC*(NS - 2)>(LPC * min(NS - 2, nck - 1 - c));
+    __builtin_amdgcn_s_barrier();
+    if (c + NS - 1 < nck) issue(c + NS - 1);
+    const bf16_t* st = smem + (c % NS) * STAGE;
+    bf16x8 wf[4], xf[4][RB];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (j < nb) {
-        const int row = j * 32 + l32;
-        const bf16x8 xf = *(const bf16x8*)&Xs[row * DG_KC + ((ch ^ (row & 15)) * 8)];
-        acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[s2], xf, acc[j], 0, 0, 0);
-      }
+    for (int kk = 0; kk < 4; ++kk) {
+      const int ch = kk * 2 + lh;
+      wf[kk] = *(const bf16x8*)(st + wrow * SK_BK + ((ch ^ sww) * 8));
+#pragma unroll
+      for (int j = 0; j < RB; ++j)
+        xf[kk][j] = *(const bf16x8*)(st + (WR + xrow[j]) * SK_BK + ((ch ^ swx[j]) * 8));
+    }
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+      for (int j = 0; j < RB; ++j)
+        acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[kk], xf[kk][j], acc[j], 0, 0, 0);
   }
-  // lane holds decode row j*32 + lane%32 and columns n0 + 8(r/4) + 4(lane/32) + r%4
+
+  // lane holds activation row xrow[j] and weight rows (output columns)
+  // n0 + strip 32 + 8 (r / 4) + 4 (lane / 32) + r % 4
+  const int nb = n0 + strip * 32;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int brow = j * 32 + l32;
-    if (j >= nb || brow >= D) continue;
-    float* out = partial + ((int64_t)split * D + brow) * N;
+  for (int j = 0; j < RB; ++j) {
+    const int row = xrow[j];
+    if constexpr (EPI == SK_ARGMAX) {
+      uint64_t best = 0;
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int n = n0 + g * 8 + lh * 4;
-      if ((N & 3) == 0 && n + 3 < N) {
-        *(float4*)(out + n) = make_float4(acc[j][g * 4], acc[j][g * 4 + 1], acc[j][g * 4 + 2],
-                                          acc[j][g * 4 + 3]);
-      } else {
+      for (int r = 0; r < 16; ++r) {
+        const int n = nb + (r >> 2) * 8 + lh * 4 + (r & 3);
+        if (n < N) {
+          const uint64_t kk = argmax_key(acc[j][r], n);
+          best = kk > best ? kk : best;
+          if (o.logits && row < D) o.logits[(int64_t)row * N + n] = acc[j][r];
+        }
+      }
+      const uint32_t plo = __shfl_xor((uint32_t)best, 32, 64);
+      const uint32_t phi = __shfl_xor((uint32_t)(best >> 32), 32, 64);
+      const uint64_t other = ((uint64_t)phi << 32) | plo;
+      best = other > best ? other : best;
+      const int n_tiles = (N + 31) / 32;
+      if (lane < 32 && row < D && nb < N) o.keys[(int64_t)row * n_tiles + nb / 32] = best;
+    } else {
+      if (row >= D) continue;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (n + i < N) out[n + i] = acc[j][g * 4 + i];
+      for (int g = 0; g < 4; ++g) {
+        const int n = nb + g * 8 + lh * 4;
+        float4 v = make_float4(acc[j][g * 4], acc[j][g * 4 + 1], acc[j][g * 4 + 2],
+                               acc[j][g * 4 + 3]);
+        if constexpr (EPI == SK_PARTIAL) {
+          *(float4*)((float*)o.out + ((int64_t)split * D + row) * N + n) = v;
+        } else {
+          v = add4(v, *(const float4*)(o.bias + n));
+          if constexpr (EPI == SK_GELU) v = gelu4(v);
+          typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+          u32x2 u;
+          u.x = pack2_bf16(v.x, v.y);
+          u.y = pack2_bf16(v.z, v.w);
+          *(u32x2*)((bf16_t*)o.out + (int64_t)row * N + n) = u;
+        }
       }
     }
   }
 }
 
-int dgemm_splits(int K) { return K / DG_KC; }
-
-int dgemm_bf16(const bf16_t* x, const bf16_t* w, int D, int N, int K, float* partial,
-               int max_splits, hipStream_t s) {
-  const int splits = K / DG_KC;                     // K is a multiple of 128 (checked at create)
-  if (splits > max_splits || D <= 0) return splits;
-  dim3 grid((N + 127) / 128, splits);
-  k_dgemm_bf16<<<grid, 256, 0, s>>>(x, w, D, N, K, partial);
-  return splits;
+template <int WN, int NS, int EPI>
+static void launch_skinny(const bf16_t* x, const bf16_t* w, int D, int N, int K, int splits,
+                          const SkOut& o, hipStream_t s) {
+  constexpr size_t lds = (size_t)NS * (32 * WN + 128) * SK_BK * sizeof(bf16_t);
+  static_assert(lds <= 160 * 1024, "LDS");
+  auto kfn = k_skinny_bf16<WN, NS, EPI>;
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)lds);
+    attr = true;
+  }
+  dim3 grid((N + 32 * WN - 1) / (32 * WN), splits);
+  kfn<<<grid, 256, lds, s>>>(x, w, D, N, K, K / splits, o);
 }
 
-int dgemm_f32(const float* x, const float* w, int D, int N, int K, float* partial,
-              int max_splits, hipStream_t s) {
-  (void)max_splits;
+// K slices of a partial-sum product: the largest divisor of K / 64 that keeps
+// the grid (N / 32 strips x slices) within one block per CU, at most 16.
+int dgemm_splits(int N, int K) {
+  const int tiles = N / 32, q = K / 64;
+  int best = 1;
+  for (int sp = 1; sp <= 16 && sp <= q; ++sp)
+    if (q % sp == 0 && tiles * sp <= 256) best = sp;
+  return best;
+}
+
+int dgemm_bf16(const bf16_t* x, const bf16_t* w, int D, int N, int K, int epi,
+               const float* bias, void* out, hipStream_t s) {
+  // N % 32 == 0, K % 64 == 0 and D <= 128 are checked when the context is created
+  if (D <= 0) return 1;
+  SkOut o{out, bias, nullptr, nullptr};
+  // three stages (two 20-KB chunks in flight per block): deeper rings measure
+  // no faster at these sizes, where launch ramp-up and drain dominate
+  if (epi == DG_PARTIAL) {
+    const int sp = dgemm_splits(N, K);
+    launch_skinny<1, 3, SK_PARTIAL>(x, w, D, N, K, sp, o, s);
+    return sp;
+  }
+  if (epi == DG_GELU)
+    launch_skinny<1, 3, SK_GELU>(x, w, D, N, K, 1, o, s);
+  else
+    launch_skinny<1, 3, SK_BIAS>(x, w, D, N, K, 1, o, s);
+  return 1;
+}
+
+void dgemm_f32(const float* x, const float* w, int D, int N, int K, float* out, hipStream_t s) {
   AView a{x, K, 0, 1 << 30};
   Epilogue e{};
   e.kind = EPI_STORE;
-  e.out = partial;
+  e.out = out;
   e.ldc = N;
   gemm_f32(a, w, D, N, K, e, s);
-  return 1;
 }
 
 template <typename T>
@@ -1554,6 +1666,16 @@ __global__ __launch_bounds__(1024) void k_reduce_resid_ln(const float* __restric
   const int grp = tid % G, sg = tid / G;
   const int64_t rs = (int64_t)D * d;                 // stride between splits
   const float* src = partial + (int64_t)b * d + grp * 4;
+  // the owners' row, bias and LayerNorm parameters load beside the partials
+  // (one memory round trip for the whole kernel)
+  float4 hv = make_float4(0.f, 0.f, 0.f, 0.f), bv = hv, gg = hv, bb = hv;
+  float* hp = h + (int64_t)b * d + tid * 4;
+  if (tid < G) {
+    hv = *(const float4*)hp;
+    bv = *(const float4*)(bias + tid * 4);
+    gg = *(const float4*)(g + tid * 4);
+    bb = *(const float4*)(beta + tid * 4);
+  }
   float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
   if (sg < SG) {
     int s = sg;
@@ -1572,8 +1694,7 @@ __global__ __launch_bounds__(1024) void k_reduce_resid_ln(const float* __restric
   float sum = 0.f;
   if (tid < G) {
     for (int k = 1; k < SG; ++k) a = add4(a, part[tid + k * G]);
-    float* hp = h + (int64_t)b * d + tid * 4;
-    v = add4(add4(*(const float4*)hp, *(const float4*)(bias + tid * 4)), a);
+    v = add4(add4(hv, bv), a);
     *(float4*)hp = v;
     sum = (v.x + v.y) + (v.z + v.w);
   }
@@ -1596,7 +1717,6 @@ __global__ __launch_bounds__(1024) void k_reduce_resid_ln(const float* __restric
   for (int w2 = 0; w2 < nw; ++w2) var += red[1][w2];
   const float rstd = rsqrtf(var / d + 1e-5f);
   if (tid < G) {
-    const float4 gg = *(const float4*)(g + tid * 4), bb = *(const float4*)(beta + tid * 4);
     const float o[4] = {(v.x - mean) * rstd * gg.x + bb.x, (v.y - mean) * rstd * gg.y + bb.y,
                         (v.z - mean) * rstd * gg.z + bb.z, (v.w - mean) * rstd * gg.w + bb.w};
 #pragma unroll
@@ -1623,69 +1743,16 @@ template void reduce_resid_ln<bf16_t>(const float*, int, int, int, const float*,
 // ---------------------------------------------------------------------------
 int vocab_tiles(int V) { return (V + 31) / 32; }
 
-// Larger key = larger value, then lower index.  Any NaN gets the largest
-// value key so that it always wins and the finishing pass reports it.
-__device__ __forceinline__ uint64_t argmax_key(float v, int n) {
-  uint32_t o = (v != v) ? 0xffffffffu : ordered_u32(v);
-  return ((uint64_t)o << 32) | (uint64_t)(0xffffffffu - (uint32_t)n);
-}
-
-// One block: 128 vocabulary rows (one wave per 32) x all decode rows.  Each
-// vocabulary row is read once; each wave leaves, for every decode row, the
-// best key over its 32 vocabulary rows (tile = 32 rows).
-__global__ __launch_bounds__(256) void k_vocab_bf16(const bf16_t* __restrict__ x,
-                                                    const bf16_t* __restrict__ emb, int D, int V,
-                                                    int K, uint64_t* keys, int n_tiles,
-                                                    float* logits) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int tile = blockIdx.x * 4 + wave;
-  const int n0 = tile * 32;
-  if (n0 >= V) return;
-  const int lk = (lane >> 5) * 8, l32 = lane & 31;
-  const int nb = (D + 31) / 32;
-  const bf16_t* wp = emb + (int64_t)min(n0 + l32, V - 1) * K + lk;
-  const bf16_t* xp[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) xp[j] = x + (int64_t)min(j * 32 + l32, D - 1) * K + lk;
-  f32x16 acc[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
-  for (int k = 0; k < K; k += 16) {
-    const bf16x8 wf = *(const bf16x8*)(wp + k);
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (j < nb) {
-        const bf16x8 xf = *(const bf16x8*)(xp[j] + k);
-        acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf, xf, acc[j], 0, 0, 0);
-      }
-  }
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    if (j >= nb) continue;
-    const int brow = j * 32 + l32;
-    uint64_t best = 0;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int n = n0 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-      if (n < V) {
-        const uint64_t kk = argmax_key(acc[j][r], n);
-        best = kk > best ? kk : best;
-        if (logits && brow < D) logits[(int64_t)brow * V + n] = acc[j][r];
-      }
-    }
-    const uint32_t plo = __shfl_xor((uint32_t)best, 32, 64);
-    const uint32_t phi = __shfl_xor((uint32_t)(best >> 32), 32, 64);
-    const uint64_t other = ((uint64_t)phi << 32) | plo;
-    best = other > best ? other : best;
-    if (lane < 32 && brow < D) keys[(int64_t)brow * n_tiles + tile] = best;
-  }
-}
-
+// The vocabulary projection is the skinny product with 128 vocabulary rows per
+// block (each wave one 32-row strip against all 128 row slots, so the
+// activations are read once per 128 vocabulary rows); each wave leaves, for
+// each decode row, the best key over its 32-row vocabulary tile.
 void vocab_argmax_bf16(const bf16_t* x, const bf16_t* emb, int D, int V, int K, uint64_t* keys,
                        int n_tiles, float* logits, hipStream_t s) {
-  if (D > 0) k_vocab_bf16<<<(n_tiles + 3) / 4, 256, 0, s>>>(x, emb, D, V, K, keys, n_tiles, logits);
+  if (D <= 0) return;
+  (void)n_tiles;   // = vocab_tiles(V): the kernel derives it from V
+  SkOut o{nullptr, nullptr, keys, logits};
+  launch_skinny<4, 4, SK_ARGMAX>(x, emb, D, V, K, 1, o, s);
 }
 
 void vocab_logits_f32(const float* x, const float* emb, int D, int V, int K, float* logits,

@@ -278,18 +278,31 @@ template void embed<bf16_t>(const bf16_t*, const float*, const int32_t*, const i
 constexpr int MEL_FR = 16;
 constexpr int MEL_SEG = (MEL_FR - 1) * kHop + kNFFT;   // 2800 samples
 
-__global__ __launch_bounds__(256) void k_log_mel(const float* const* pcm_ptrs,
-                                                 const int64_t* n_samples, int n_mels,
-                                                 MelTables tb, float* mel_raw,
-                                                 uint32_t* clip_max) {
+// Where a clip's samples are: device arrays of pointers and lengths, or the
+// same lists carried in the kernel arguments (MelClipArgs).
+struct ClipsInMemory {
+  const float* const* ptrs;
+  const int64_t* n;
+  __device__ const float* ptr(int i) const { return ptrs[i]; }
+  __device__ int64_t len(int i) const { return n[i]; }
+};
+struct ClipsInArgs {
+  MelClipArgs a;
+  __device__ const float* ptr(int i) const { return a.ptr[i]; }
+  __device__ int64_t len(int i) const { return a.n[i]; }
+};
+
+template <class Clips>
+__global__ __launch_bounds__(256) void k_log_mel(Clips clips, int n_mels, MelTables tb,
+                                                 float* mel_raw, uint32_t* clip_max) {
   __shared__ float seg[MEL_SEG];
   __shared__ float wc[kNFFT], ws[kNFFT];
   __shared__ float pw[MEL_FR][kBins + 3];
   __shared__ float red[4];
   const int clip = blockIdx.y;
   const int f0 = blockIdx.x * MEL_FR;
-  const float* x = pcm_ptrs[clip];
-  const int64_t n = n_samples[clip];
+  const float* x = clips.ptr(clip);
+  const int64_t n = clips.len(clip);
   const int tid = threadIdx.x;
 
   for (int i = tid; i < MEL_SEG; i += 256) {
@@ -355,7 +368,16 @@ void log_mel(const float* const* pcm_ptrs, const int64_t* n_samples, int n_clips
   if (n_clips <= 0) return;
   fill_u32(clip_max, 0u, n_clips, s);
   dim3 grid((kFrames + MEL_FR - 1) / MEL_FR, n_clips);
-  k_log_mel<<<grid, 256, 0, s>>>(pcm_ptrs, n_samples, n_mels, t, mel_raw, clip_max);
+  k_log_mel<ClipsInMemory><<<grid, 256, 0, s>>>(ClipsInMemory{pcm_ptrs, n_samples}, n_mels, t,
+                                                mel_raw, clip_max);
+}
+
+void log_mel_args(const MelClipArgs& clips, int n_clips, int n_mels, const MelTables& t,
+                  float* mel_raw, uint32_t* clip_max, hipStream_t s) {
+  if (n_clips <= 0) return;
+  fill_u32(clip_max, 0u, n_clips, s);
+  dim3 grid((kFrames + MEL_FR - 1) / MEL_FR, n_clips);
+  k_log_mel<ClipsInArgs><<<grid, 256, 0, s>>>(ClipsInArgs{clips}, n_mels, t, mel_raw, clip_max);
 }
 
 // Dynamic-range clamp 8 below the clip's maximum, then (x + 4) / 4.  With

@@ -84,12 +84,11 @@ struct Layout {
   size_t pcm_stage = 0, pcm_ptrs = 0, pcm_n = 0, mel_raw = 0, clip_max = 0, mel_norm = 0,
          h1 = 0, x = 0, xn = 0, qkv = 0, vt = 0, att = 0, hid = 0, p_slots = 0;
   size_t vt_bytes = 0;
-  size_t d_slots = 0, d_tokens = 0, d_pos = 0, d_h = 0, d_xn = 0, d_qkv = 0, d_q = 0, d_att = 0,
+  size_t d_slots = 0, d_tokens = 0, d_pos = 0, d_h = 0, d_xn = 0, d_qkv = 0, d_att = 0,
          d_hid = 0, d_partial = 0, d_apart = 0, d_logits = 0, d_keys = 0, d_argmax = 0,
          d_flag = 0;
   size_t wstage = 0;
   int64_t wstage_floats = 0;
-  int max_splits = 1;
   std::vector<PackOp> pack;
   std::vector<std::pair<size_t, size_t>> zero_regions;   // (offset, bytes) zeroed before packing
 };
@@ -98,6 +97,7 @@ struct TimedLaunch {
   int cls;
   hipEvent_t a, b;
   double flops, bytes;
+  int64_t inst = -1;   // >= 0: one of several end events of a phase instance (max counts)
 };
 
 }  // namespace
@@ -125,6 +125,12 @@ struct asr_ctx {
   hipEvent_t ev_efork = nullptr, ev_ejoin[kEncGroups - 1] = {};
   std::unordered_map<int64_t, Request> serving;   // admitted, not finished (audio kept
                                                   // for a re-prefill after preemption)
+  // decode steps replayed from HIP graphs, one per (rows, logits wanted),
+  // captured on a private stream at the second step of that shape
+  bool decode_graphs = true;
+  hipStream_t cap_stream = nullptr;
+  std::unordered_map<int32_t, hipGraphExec_t> dgraph;
+  std::unordered_map<int32_t, int32_t> dshape_seen;
   Layout L;
   bool bound = false, loaded = false;
   char* base = nullptr;
@@ -134,6 +140,7 @@ struct asr_ctx {
   int32_t timing = 0;   // bit mask over asr_kernel_class
   std::vector<hipEvent_t> ev_pool;
   size_t ev_used = 0;
+  int64_t next_inst = 0;
   std::vector<TimedLaunch> pending;
   double t_ms[ASR_K_COUNT] = {}, t_flops[ASR_K_COUNT] = {}, t_bytes[ASR_K_COUNT] = {};
   int64_t t_n[ASR_K_COUNT] = {};
@@ -306,16 +313,19 @@ void plan(asr_ctx* c) {
   L.d_h = b.take(D * d * f4);
   L.d_xn = b.take(D * std::max<int64_t>(d, F) * es);
   L.d_qkv = b.take(D * 3 * d * es);
-  L.d_q = b.take(D * d * es);
   L.d_att = b.take(D * d * es);
   L.d_hid = b.take(D * F * es);
-  // split-K partial sums: the bf16 decode GEMM splits K in 128-deep slices
-  L.max_splits = c->cfg.dtype == ASR_BF16 ? std::max(dgemm_splits(F), dgemm_splits(d)) : 1;
+  // partial sums of the decode products: the bf16 path splits the K range of
+  // the products whose output feeds a residual LayerNorm or the cross
+  // attention (N = d); the fp32 path holds one slice of any product
   {
-    int64_t most = std::max<int64_t>((int64_t)dgemm_splits(d) * std::max<int64_t>(3 * d, F),
-                                     (int64_t)dgemm_splits(F) * d);
-    if (c->cfg.dtype != ASR_BF16) most = Nmax;
-    L.d_partial = b.take(std::max<int64_t>(most, Nmax) * D * f4);
+    int64_t most = D * std::max<int64_t>(3 * d, F);
+    if (c->cfg.dtype == ASR_BF16)
+      most = std::max<int64_t>(
+          most, std::max<int64_t>(D * d * std::max(dgemm_splits((int)d, (int)d),
+                                                   dgemm_splits((int)d, (int)F)),
+                                  D * 3 * d * dgemm_splits((int)(3 * d), (int)d)));
+    L.d_partial = b.take(most * f4);
   }
   L.d_apart = b.take((int64_t)decode_attn_part_floats((int)D, g.n_head) * f4);
   L.d_logits = b.take(D * (int64_t)std::max(1, g.vocab) * f4);
@@ -346,17 +356,26 @@ double slaney_hz(double m) {
   return m < min_log_mel ? m * f_sp : min_log_hz * std::exp(logstep * (m - min_log_mel));
 }
 
-asr_status upload_tables(asr_ctx* c) {
-  const int M = c->cfg.n_mels, d = c->cfg.d_model;
-  std::vector<float> win(kNFFT), ct(kNFFT), st(kNFFT);
+// Window, twiddles, mel filterbank (Slaney scale, area-normalised triangles
+// over the 201 bins) and each filter's nonzero bin range.
+struct HostMelTables {
+  std::vector<float> win, ct, st, fb;
+  std::vector<int32_t> rng;
+};
+
+HostMelTables host_mel_tables(int M) {
+  HostMelTables t;
+  t.win.resize(kNFFT);
+  t.ct.resize(kNFFT);
+  t.st.resize(kNFFT);
   for (int i = 0; i < kNFFT; ++i) {
     double a = 2.0 * M_PI * i / kNFFT;
-    win[i] = (float)(0.5 - 0.5 * std::cos(a));
-    ct[i] = (float)std::cos(a);
-    st[i] = (float)std::sin(a);
+    t.win[i] = (float)(0.5 - 0.5 * std::cos(a));
+    t.ct[i] = (float)std::cos(a);
+    t.st[i] = (float)std::sin(a);
   }
-  std::vector<float> fb((size_t)M * kBins, 0.f);
-  std::vector<int32_t> rng((size_t)M * 2, 0);
+  t.fb.assign((size_t)M * kBins, 0.f);
+  t.rng.assign((size_t)M * 2, 0);
   std::vector<double> edge(M + 2);
   double mlo = slaney_mel(0.0), mhi = slaney_mel(kSampleRate / 2.0);
   for (int i = 0; i < M + 2; ++i) edge[i] = slaney_hz(mlo + (mhi - mlo) * i / (M + 1));
@@ -368,15 +387,23 @@ asr_status upload_tables(asr_ctx* c) {
       double up = (f - edge[m]) / (edge[m + 1] - edge[m]);
       double down = (edge[m + 2] - f) / (edge[m + 2] - edge[m + 1]);
       double w = std::max(0.0, std::min(up, down)) * norm;
-      fb[(size_t)m * kBins + k] = (float)w;
+      t.fb[(size_t)m * kBins + k] = (float)w;
       if (w > 0) {
         if (first < 0) first = k;
         last = k;
       }
     }
-    rng[2 * m] = first < 0 ? 0 : first;
-    rng[2 * m + 1] = first < 0 ? 0 : last - first + 1;
+    t.rng[2 * m] = first < 0 ? 0 : first;
+    t.rng[2 * m + 1] = first < 0 ? 0 : last - first + 1;
   }
+  return t;
+}
+
+asr_status upload_tables(asr_ctx* c) {
+  const int M = c->cfg.n_mels, d = c->cfg.d_model;
+  const HostMelTables mt = host_mel_tables(M);
+  const std::vector<float>&win = mt.win, &ct = mt.ct, &st = mt.st, &fb = mt.fb;
+  const std::vector<int32_t>& rng = mt.rng;
   std::vector<float> sin_tab((size_t)kCtx * d);
   const int half = d / 2;
   const double inc = std::log(10000.0) / (half - 1);
@@ -451,14 +478,27 @@ struct PhaseMark {
 
 asr_status collect_timing(asr_ctx* c) {
   if (c->pending.empty()) return ASR_OK;
-  HIPCHK(hipStreamSynchronize(c->stream));
+  HIPCHK(hipDeviceSynchronize());
+  std::unordered_map<int64_t, std::pair<int, float>> inst_ms;   // instance -> (class, max ms)
   for (auto& p : c->pending) {
     float ms = 0.f;
     HIPCHK(hipEventElapsedTime(&ms, p.a, p.b));
+    if (p.inst >= 0) {
+      auto it = inst_ms.find(p.inst);
+      if (it == inst_ms.end())
+        inst_ms[p.inst] = {p.cls, ms};
+      else
+        it->second.second = std::max(it->second.second, ms);
+      continue;
+    }
     c->t_ms[p.cls] += ms;
     c->t_n[p.cls] += 1;
     c->t_flops[p.cls] += p.flops;
     c->t_bytes[p.cls] += p.bytes;
+  }
+  for (auto& kv : inst_ms) {
+    c->t_ms[kv.second.first] += kv.second.second;
+    c->t_n[kv.second.first] += 1;
   }
   c->pending.clear();
   c->ev_used = 0;
@@ -552,6 +592,23 @@ asr_status encode_clips(asr_ctx* c, int n, bool xkv = false) {
   const asr_model_cfg& g = c->cfg;
   const int d = g.d_model, F = g.d_ffn, Mm = g.n_mels, H = g.n_head;
   const Layout& L = c->L;
+  // the encoder phase (mel .. ln_post): starts here on the bound stream and
+  // ends when the last clip group has its ln_post output
+  hipEvent_t enc_a = nullptr;
+  const int64_t enc_inst = c->next_inst++;
+  if (c->timing >> ASR_K_ENCODE & 1) {
+    enc_a = next_event(c);
+    if (enc_a) (void)hipEventRecord(enc_a, c->stream);
+  }
+  auto enc_end = [&]() {
+    if (!enc_a) return;
+    hipEvent_t b = next_event(c);
+    if (!b) return;
+    (void)hipEventRecord(b, c->stream);
+    TimedLaunch t{ASR_K_ENCODE, enc_a, b, 0.0, 0.0};
+    t.inst = enc_inst;
+    c->pending.push_back(t);
+  };
   asr_status st = run_mel(c, n);
   if (st != ASR_OK) return st;
   timed(c, ASR_K_MEL, 0.0, (double)n * kFrames * Mm * (4 + c->es), [&] {
@@ -686,6 +743,7 @@ asr_status encode_clips(asr_ctx* c, int n, bool xkv = false) {
       const bool last = l == g.n_enc;
       res_ln_any<T>(c, x, y, R, last ? L.lnp_g : L.enc[l].ln1_g,
                     last ? L.lnp_b : L.enc[l].ln1_b, xn);
+      if (last) enc_end();
       if (last && xkv) {
         const asr_status st2 = cross_kv<T>(c, xn, ng, clip0[grp]);
         if (st2 != ASR_OK) {
@@ -702,6 +760,7 @@ asr_status encode_clips(asr_ctx* c, int n, bool xkv = false) {
   }
   if (g.n_enc == 0) {
     ln_any<T>(c, x_all, n * kCtx, L.lnp_g, L.lnp_b, xn_all);
+    enc_end();
     if (xkv) {
       const asr_status st2 = cross_kv<T>(c, xn_all, n, 0);
       if (st2 != ASR_OK) return st2;
@@ -734,41 +793,51 @@ asr_status cross_kv(asr_ctx* c, const void* E, int n, int slot0) {
 // ---------------------------------------------------------------------------
 // Decode pipeline (rows already uploaded to d_slots / d_tokens / d_pos)
 // ---------------------------------------------------------------------------
+// Decode product with its epilogue: out = (GELU)(x W^T + bias) in the
+// storage type.  bf16: one kernel; fp32: the product, then the epilogue.
 template <typename T>
-void dgemm_any(asr_ctx* c, const T* x, size_t w_off, int D, int N, int K, size_t bias_off,
-               int mode, void* out) {
+void dgemm_out(asr_ctx* c, const T* x, size_t w_off, int D, int N, int K, size_t bias_off,
+               bool gelu, T* out) {
   float* part = c->at<float>(c->L.d_partial);
-  int splits = 1;
-  double bytes = (double)N * K * c->es + (double)D * K * c->es + (double)D * N * c->es;
+  const double bytes = (double)N * K * c->es + (double)D * K * c->es + (double)D * N * c->es;
   timed(c, ASR_K_DGEMM, 2.0 * D * N * K, bytes, [&] {
-    if (c->bf16())
-      splits = dgemm_bf16((const bf16_t*)x, c->at<bf16_t>(w_off), D, N, K, part,
-                          c->L.max_splits, c->stream);
-    else
-      splits = dgemm_f32((const float*)x, c->at<float>(w_off), D, N, K, part,
-                         c->L.max_splits, c->stream);
-    dgemm_reduce<T>(part, splits, D, N, c->at<float>(bias_off), mode, out, c->stream);
+    if (c->bf16()) {
+      dgemm_bf16((const bf16_t*)x, c->at<bf16_t>(w_off), D, N, K, gelu ? DG_GELU : DG_BIAS,
+                 c->at<float>(bias_off), out, c->stream);
+    } else {
+      dgemm_f32((const float*)x, c->at<float>(w_off), D, N, K, part, c->stream);
+      dgemm_reduce<T>(part, 1, D, N, c->at<float>(bias_off), gelu ? 1 : 0, out, c->stream);
+    }
   });
 }
 
-// Residual product (N = d) whose split-K reduce also adds the residual into h
-// and writes the next LayerNorm (g, b) of h into xn.
+// Decode product left as float32 partial sums over K slices in d_partial
+// (the consumer adds the slices and the bias); returns the slice count.
+template <typename T>
+int dgemm_part(asr_ctx* c, const T* x, size_t w_off, int D, int N, int K) {
+  float* part = c->at<float>(c->L.d_partial);
+  int splits = 1;
+  const double bytes = (double)N * K * c->es + (double)D * K * c->es + (double)D * N * c->es;
+  timed(c, ASR_K_DGEMM, 2.0 * D * N * K, bytes, [&] {
+    if (c->bf16())
+      splits = dgemm_bf16((const bf16_t*)x, c->at<bf16_t>(w_off), D, N, K, DG_PARTIAL, nullptr,
+                          part, c->stream);
+    else
+      dgemm_f32((const float*)x, c->at<float>(w_off), D, N, K, part, c->stream);
+  });
+  return splits;
+}
+
+// Residual product (N = d): h += bias + x W^T, then xn = LayerNorm(h) with
+// (g, b) -- the product's K slices are added by the LayerNorm kernel.
 template <typename T>
 void dgemm_resid_ln(asr_ctx* c, const T* x, size_t w_off, int D, int K, size_t bias_off,
                     float* h, size_t g_off, size_t b_off, T* xn) {
   const int d = c->cfg.d_model;
-  float* part = c->at<float>(c->L.d_partial);
-  int splits = 1;
-  double bytes = (double)d * K * c->es + (double)D * K * c->es + (double)D * d * (8 + c->es);
-  timed(c, ASR_K_DGEMM, 2.0 * D * d * K, bytes, [&] {
-    if (c->bf16())
-      splits = dgemm_bf16((const bf16_t*)x, c->at<bf16_t>(w_off), D, d, K, part,
-                          c->L.max_splits, c->stream);
-    else
-      splits = dgemm_f32((const float*)x, c->at<float>(w_off), D, d, K, part,
-                         c->L.max_splits, c->stream);
-    reduce_resid_ln<T>(part, splits, D, d, c->at<float>(bias_off), h, c->at<float>(g_off),
-                       c->at<float>(b_off), xn, c->stream);
+  const int splits = dgemm_part<T>(c, x, w_off, D, d, K);
+  timed(c, ASR_K_LN, 9.0 * D * d, (double)D * d * (4.0 * splits + 8 + c->es), [&] {
+    reduce_resid_ln<T>(c->at<float>(c->L.d_partial), splits, D, d, c->at<float>(bias_off), h,
+                       c->at<float>(g_off), c->at<float>(b_off), xn, c->stream);
   });
 }
 
@@ -780,7 +849,6 @@ asr_status decode_rows(asr_ctx* c, int D, const std::vector<int32_t>& pos_host, 
   float* h = c->at<float>(L.d_h);
   T* xn = c->at<T>(L.d_xn);
   T* qkv = c->at<T>(L.d_qkv);
-  T* q = c->at<T>(L.d_q);
   T* att = c->at<T>(L.d_att);
   T* hid = c->at<T>(L.d_hid);
   const int32_t* slots = c->at<int32_t>(L.d_slots);
@@ -797,23 +865,30 @@ asr_status decode_rows(asr_ctx* c, int D, const std::vector<int32_t>& pos_host, 
   ln_any<T>(c, h, D, L.dec[0].ln1_g, L.dec[0].ln1_b, xn);
   for (int l = 0; l < g.n_dec; ++l) {
     const DecLayer& w = L.dec[l];
-    // xn holds LN_attn(h) here
-    dgemm_any<T>(c, xn, w.qkv_w, D, 3 * d, d, w.qkv_b, 0, qkv);
+    // xn holds LN_attn(h) here; bf16: the QKV product stays in K-slice
+    // partial sums that the self-attention kernel adds up with the bias
+    int qkv_splits = 0;
+    if (c->bf16())
+      qkv_splits = dgemm_part<T>(c, xn, w.qkv_w, D, 3 * d, d);
+    else
+      dgemm_out<T>(c, xn, w.qkv_w, D, 3 * d, d, w.qkv_b, false, qkv);
     const int64_t self_off = (int64_t)l * 2 * H * kTextCtx * kHeadDim;
     timed(c, ASR_K_DATTN, 4.0 * self_keys * 64 * H, self_keys * 2 * 64 * H * c->es, [&] {
-      decode_self_attn<T>(qkv, self_cache, L.self_stride, self_off, slots, pos, D, H, att,
+      decode_self_attn<T>(qkv, c->at<float>(L.d_partial), qkv_splits, c->at<float>(w.qkv_b),
+                          self_cache, L.self_stride, self_off, slots, pos, D, H, att,
                           c->at<float>(L.d_apart), c->stream);
     });
     dgemm_resid_ln<T>(c, att, w.o_w, D, d, w.o_b, h, w.lnx_g, w.lnx_b, xn);
-    dgemm_any<T>(c, xn, w.xq_w, D, d, d, w.xq_b, 0, q);
+    const int q_splits = dgemm_part<T>(c, xn, w.xq_w, D, d, d);
     const int64_t cross_off = (int64_t)l * 2 * H * kCtx * kHeadDim;
     timed(c, ASR_K_DATTN, 4.0 * D * H * (double)kCtx * 64, (double)D * H * kCtx * 2 * 64 * c->es,
           [&] {
-            decode_cross_attn<T>(q, cross_cache, L.cross_stride, cross_off, slots, D, H, att,
+            decode_cross_attn<T>(c->at<float>(L.d_partial), q_splits, c->at<float>(w.xq_b),
+                                 cross_cache, L.cross_stride, cross_off, slots, D, H, att,
                                  c->at<float>(L.d_apart), c->stream);
           });
     dgemm_resid_ln<T>(c, att, w.xo_w, D, d, w.xo_b, h, w.ln2_g, w.ln2_b, xn);
-    dgemm_any<T>(c, xn, w.fc1_w, D, F, d, w.fc1_b, 1, hid);
+    dgemm_out<T>(c, xn, w.fc1_w, D, F, d, w.fc1_b, true, hid);
     // the last residual of the layer also produces the next LayerNorm input
     const bool last = l + 1 == g.n_dec;
     dgemm_resid_ln<T>(c, hid, w.fc2_w, D, F, w.fc2_b, h, last ? L.lnf_g : L.dec[l + 1].ln1_g,
@@ -926,6 +1001,8 @@ asr_status asr_destroy(asr_ctx* c) {
       if (c->estream[i]) (void)hipStreamDestroy(c->estream[i]);
     }
     if (c->ev_efork) (void)hipEventDestroy(c->ev_efork);
+    for (auto& kv : c->dgraph) (void)hipGraphExecDestroy(kv.second);
+    if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
   }
   delete c;
   return ASR_OK;
@@ -943,6 +1020,9 @@ asr_status asr_bind(asr_ctx* c, void* dev_block, size_t bytes, void* stream) {
   if (!dev_block || ((uintptr_t)dev_block & 255)) return fail(ASR_EINVAL, "block must be 256-byte aligned");
   if (bytes < c->L.total) return fail(ASR_ENOMEM, "bound block smaller than asr_workspace_size");
   HIPCHK(hipSetDevice(c->device));
+  for (auto& kv : c->dgraph) (void)hipGraphExecDestroy(kv.second);
+  c->dgraph.clear();
+  c->dshape_seen.clear();
   c->base = (char*)dev_block;
   c->bytes = bytes;
   c->stream = (hipStream_t)stream;
@@ -1158,6 +1238,48 @@ asr_status run_prefill(asr_ctx* c, const std::vector<const Request*>& reqs,
   return st;
 }
 
+// Enqueues the decode kernels of D rows on c->stream: directly, or by
+// replaying the HIP graph of this shape.  Every argument of those kernels is
+// a device pointer or a size fixed by (D, logits wanted) -- positions, slots
+// and tokens are read from device memory -- so one graph serves every step of
+// a shape.  A shape's first step runs directly (it also performs the
+// kernels' one-time attribute set-up); the second is captured on a private
+// stream and replayed from then on.  Per-launch timing always runs directly.
+asr_status decode_launch(asr_ctx* c, int D, const std::vector<int32_t>& pos, bool want_logits) {
+  auto direct = [&]() {
+    return c->bf16() ? decode_rows<bf16_t>(c, D, pos, want_logits)
+                     : decode_rows<float>(c, D, pos, want_logits);
+  };
+  const int32_t key = D * 2 + (want_logits ? 1 : 0);
+  const bool per_launch_timing = (c->timing & ~((1 << ASR_K_PREFILL) | (1 << ASR_K_DECODE) |
+                                                (1 << ASR_K_ENCODE))) != 0;
+  if (!c->decode_graphs || per_launch_timing) return direct();
+  auto it = c->dgraph.find(key);
+  if (it == c->dgraph.end()) {
+    if (c->dshape_seen[key]++ == 0) return direct();
+    if (!c->cap_stream) HIPCHK(hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking));
+    hipStream_t bound = c->stream;
+    c->stream = c->cap_stream;
+    HIPCHK(hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal));
+    asr_status st = direct();
+    hipGraph_t g = nullptr;
+    const hipError_t e = hipStreamEndCapture(c->cap_stream, &g);
+    c->stream = bound;
+    if (st != ASR_OK) {
+      if (g) (void)hipGraphDestroy(g);
+      return st;
+    }
+    if (e != hipSuccess) return fail(ASR_EDEVICE, std::string("hipStreamEndCapture: ") + hipGetErrorString(e));
+    hipGraphExec_t ex = nullptr;
+    const hipError_t e2 = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    if (e2 != hipSuccess) return fail(ASR_EDEVICE, std::string("hipGraphInstantiate: ") + hipGetErrorString(e2));
+    it = c->dgraph.emplace(key, ex).first;
+  }
+  HIPCHK(hipGraphLaunch(it->second, c->stream));
+  return ASR_OK;
+}
+
 // Decode rows (slot, token, position) -> argmax (and logits when asked).
 // Returns EDEVICE after the copies when a NaN logit was flagged.
 asr_status run_decode(asr_ctx* c, int D, const int32_t* slots, const int32_t* tokens,
@@ -1168,8 +1290,7 @@ asr_status run_decode(asr_ctx* c, int D, const int32_t* slots, const int32_t* to
   HIPCHK(hipMemcpyAsync(c->at(c->L.d_tokens), tokens, D * 4, hipMemcpyHostToDevice, s));
   HIPCHK(hipMemcpyAsync(c->at(c->L.d_pos), pos.data(), D * 4, hipMemcpyHostToDevice, s));
   PhaseMark pm(c, ASR_K_DECODE);
-  asr_status st = c->bf16() ? decode_rows<bf16_t>(c, D, pos, logits != nullptr)
-                            : decode_rows<float>(c, D, pos, logits != nullptr);
+  asr_status st = decode_launch(c, D, pos, logits != nullptr);
   if (st != ASR_OK) return st;
   pm.end();
   int32_t flag = 0;
@@ -1526,6 +1647,12 @@ asr_status asr_serve_tokens(asr_ctx* c, int64_t id, int32_t* tokens, int32_t cap
   return ASR_OK;
 }
 
+asr_status asr_set_decode_graphs(asr_ctx* c, int32_t on) {
+  if (!c) return fail(ASR_EINVAL, "NULL context");
+  c->decode_graphs = on != 0;
+  return ASR_OK;
+}
+
 asr_status asr_set_encoder_streams(asr_ctx* c, int32_t n) {
   if (!c) return fail(ASR_EINVAL, "NULL context");
   if (n < 1 || n > asr_ctx::kEncGroups) return fail(ASR_EINVAL, "n out of [1, 4]");
@@ -1733,3 +1860,4 @@ asr_status asr_debug_set_self_kv(asr_ctx* c, int32_t slot, const float* src, int
 }
 
 }  // extern "C"
+
