@@ -11,7 +11,16 @@ from oracle import mel as OM
 from oracle import whisper as W
 from paper_2603_11273_amd import synth
 
-torch.set_default_dtype(torch.float64)
+
+
+@pytest.fixture(autouse=True)
+def _float64_default():
+    """These pins compare against torch in float64; the default dtype is
+    restored afterwards so that other test modules keep torch's float32."""
+    old = torch.get_default_dtype()
+    torch.set_default_dtype(torch.float64)
+    yield
+    torch.set_default_dtype(old)
 
 
 def test_gelu_layernorm_match_torch():
