@@ -376,6 +376,29 @@ asr_status asr_debug_get_kv(asr_ctx* ctx, int32_t slot, int32_t which, float* ou
 asr_status asr_debug_set_self_kv(asr_ctx* ctx, int32_t slot, const float* src, int32_t length,
                                  int32_t on_device);
 
+/* ---- allocation-free variant ------------------------------------------
+ * For callers that cannot allocate device memory or bind a workspace (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the log-mel front-end of asr_debug_logmel with its scratch in
+ * a file-scope device array of the library (192 KiB per GPU, held until the
+ * process ends) instead of a bound block.  Needs no context.
+ *   pcm[i]: device pointer to clip i's float32 samples (n_samples[i] in
+ *   [0, 480000]; may be NULL when 0); pcm and n_samples are host arrays of n
+ *   entries, n in [1, 64].  n_mels: 80 or 128.  out: device float32
+ *   [n][3000][n_mels], the normalised features (the same values
+ *   asr_debug_logmel returns).  Work is enqueued on `stream` (NULL = default
+ *   stream) of the current device; the call does not synchronise.
+ * No allocation and no per-call copy: the clip list travels in the kernel
+ * arguments.  The first call on a device resolves the array's address and
+ * uploads the constant tables with synchronous copies, so a caller that
+ * captures graphs makes one call before capturing.  All calls on one GPU
+ * share its array (the per-clip maxima are cleared at the start of every
+ * call): calls that overlap on one GPU race.
+ * Errors: EINVAL (NULL argument, n or n_mels out of range, n_samples out of
+ * range), EDEVICE (HIP error). */
+asr_status asr_logmel_noalloc(const float* const* pcm, const int64_t* n_samples, int32_t n,
+                              int32_t n_mels, float* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

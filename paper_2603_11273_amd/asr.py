@@ -33,7 +33,7 @@ EXPORTED = [
     "asr_reset_timing",
     "asr_debug_logmel", "asr_debug_encode", "asr_debug_attention", "asr_debug_set_encoder_out",
     "asr_debug_get_kv",
-    "asr_debug_set_self_kv", "asr_serve_config", "asr_serve_step",
+    "asr_debug_set_self_kv", "asr_logmel_noalloc", "asr_serve_config", "asr_serve_step",
     "asr_serve_plan",
     "asr_serve_tokens", "asr_serve_simulate", "asr_serve_stats",
 ]
@@ -125,6 +125,7 @@ def _load():
         "asr_debug_set_encoder_out": [vp, P(i32), P(i64), P(i32), i32, vp, i32],
         "asr_debug_get_kv": [vp, i32, i32, P(f)],
         "asr_debug_set_self_kv": [vp, i32, vp, i32, i32],
+        "asr_logmel_noalloc": [P(vp), P(i64), i32, i32, vp, vp],
         "asr_serve_config": [vp, P(ServeCfg)],
         "asr_serve_step": [vp, i64, P(ServeOut)],
         "asr_serve_plan": [vp, i64, P(ServeOut)],
@@ -167,6 +168,24 @@ def _i64(a):
 def _i32(a):
     a = np.ascontiguousarray(a, dtype=np.int32)
     return a, a.ctypes.data_as(C.POINTER(C.c_int32))
+
+
+def logmel_noalloc(clips, n_mels, out, stream=None):
+    """asr_logmel_noalloc: normalised log-mel features of device clips (torch
+    tensors, float32) into the device tensor out [n][3000][n_mels], on
+    `stream` (torch.cuda.Stream; default: torch's current stream)."""
+    import torch
+    n = len(clips)
+    for x in clips:
+        if not (x.is_cuda and x.dtype == torch.float32):
+            raise TypeError("clips must be float32 device tensors")
+    if not (out.is_cuda and out.dtype == torch.float32 and tuple(out.shape) == (n, 3000, n_mels)):
+        raise TypeError(f"out must be a float32 device tensor of shape ({n}, 3000, {n_mels})")
+    ptrs = (C.c_void_p * n)(*[_ptr(x) for x in clips])
+    ns = np.array([x.numel() for x in clips], np.int64)
+    st = (stream or torch.cuda.current_stream()).cuda_stream
+    _check(lib.asr_logmel_noalloc(ptrs, ns.ctypes.data_as(C.POINTER(C.c_int64)), n, n_mels,
+                                  _ptr(out), st))
 
 
 def model_cfg(shape, max_slots=8, max_prefill=1, max_decode=8, max_queue=4096) -> ModelCfg:

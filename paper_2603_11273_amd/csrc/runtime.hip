@@ -5,6 +5,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <unordered_map>
 #include <vector>
@@ -1861,3 +1862,91 @@ asr_status asr_debug_set_self_kv(asr_ctx* c, int32_t slot, const float* src, int
 
 }  // extern "C"
 
+// ===========================================================================
+// Allocation-free log-mel front-end (asr_logmel_noalloc)
+//
+// The scratch the front-end needs -- the window and twiddle tables, the mel
+// filterbanks of both supported widths with their bin ranges, and the
+// per-clip maxima of one call -- lives in a file-scope device array instead
+// of a bound block.  Host code never names that array directly: each device
+// resolves its own copy's address once (hipGetSymbolAddress, with that
+// device current) and every launch takes that address.
+// ===========================================================================
+namespace {
+
+constexpr int kNaDevices = 64;
+// word offsets into the scratch array
+constexpr size_t kNaWin = 0, kNaCos = kNaWin + kNFFT, kNaSin = kNaCos + kNFFT;
+constexpr size_t kNaFb80 = kNaSin + kNFFT, kNaFb128 = kNaFb80 + (size_t)80 * kBins;
+constexpr size_t kNaRng80 = kNaFb128 + (size_t)128 * kBins, kNaRng128 = kNaRng80 + 2 * 80;
+constexpr size_t kNaMax = kNaRng128 + 2 * 128;
+constexpr size_t kNaWords = kNaMax + kMelArgClips;
+constexpr size_t kNaBytes = 192 * 1024;   // the stated maximum: 192 KiB per GPU
+static_assert(kNaWords * 4 <= kNaBytes, "scratch layout");
+
+}  // namespace
+
+static __device__ __align__(256) uint32_t scratch[kNaBytes / 4];
+
+namespace {
+
+std::mutex g_na_mu;
+uint32_t* g_na_ptr[kNaDevices] = {};
+
+// First call on a device (that device current): resolve the array's address
+// and upload the constant tables with synchronous copies.
+asr_status na_setup(int dev, uint32_t** out) {
+  std::lock_guard<std::mutex> lock(g_na_mu);
+  if (!g_na_ptr[dev]) {
+    void* p = nullptr;
+    HIPCHK(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(ASR_EDEVICE, "hipGetSymbolAddress returned NULL");
+    uint32_t* base = (uint32_t*)p;
+    const HostMelTables t80 = host_mel_tables(80), t128 = host_mel_tables(128);
+    HIPCHK(hipMemcpy(base + kNaWin, t80.win.data(), kNFFT * 4, hipMemcpyHostToDevice));
+    HIPCHK(hipMemcpy(base + kNaCos, t80.ct.data(), kNFFT * 4, hipMemcpyHostToDevice));
+    HIPCHK(hipMemcpy(base + kNaSin, t80.st.data(), kNFFT * 4, hipMemcpyHostToDevice));
+    HIPCHK(hipMemcpy(base + kNaFb80, t80.fb.data(), t80.fb.size() * 4, hipMemcpyHostToDevice));
+    HIPCHK(hipMemcpy(base + kNaFb128, t128.fb.data(), t128.fb.size() * 4, hipMemcpyHostToDevice));
+    HIPCHK(hipMemcpy(base + kNaRng80, t80.rng.data(), t80.rng.size() * 4, hipMemcpyHostToDevice));
+    HIPCHK(hipMemcpy(base + kNaRng128, t128.rng.data(), t128.rng.size() * 4,
+                     hipMemcpyHostToDevice));
+    g_na_ptr[dev] = base;
+  }
+  *out = g_na_ptr[dev];
+  return ASR_OK;
+}
+
+}  // namespace
+
+extern "C" asr_status asr_logmel_noalloc(const float* const* pcm, const int64_t* n_samples,
+                                         int32_t n, int32_t n_mels, float* out, void* stream) {
+  if (!pcm || !n_samples || !out) return fail(ASR_EINVAL, "NULL argument");
+  if (n < 1 || n > kMelArgClips)
+    return fail(ASR_EINVAL, "n out of [1, " + std::to_string(kMelArgClips) + "] (scratch limit)");
+  if (n_mels != 80 && n_mels != 128) return fail(ASR_EINVAL, "n_mels must be 80 or 128");
+  MelClipArgs clips{};
+  for (int i = 0; i < n; ++i) {
+    if (n_samples[i] < 0 || n_samples[i] > kSamples30s)
+      return fail(ASR_EINVAL, "n_samples out of [0, 480000]");
+    if (n_samples[i] > 0 && !pcm[i]) return fail(ASR_EINVAL, "NULL pcm");
+    clips.ptr[i] = pcm[i];
+    clips.n[i] = n_samples[i];
+  }
+  int dev = -1;
+  HIPCHK(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kNaDevices) return fail(ASR_EINVAL, "device index out of range");
+  uint32_t* base = nullptr;
+  asr_status st = na_setup(dev, &base);
+  if (st != ASR_OK) return st;
+  const bool wide = n_mels == 128;
+  MelTables t{(const float*)(base + kNaWin), (const float*)(base + kNaCos),
+              (const float*)(base + kNaSin), (const float*)(base + (wide ? kNaFb128 : kNaFb80)),
+              (const int32_t*)(base + (wide ? kNaRng128 : kNaRng80))};
+  hipStream_t s = (hipStream_t)stream;
+  // raw log-mel straight into out, then the clamp and affine in place
+  log_mel_args(clips, n, n_mels, t, out, base + kNaMax, s);
+  mel_normalize<float>(out, base + kNaMax, n, n_mels, out, 0, s);
+  CHECK_LAUNCH();
+  return ASR_OK;
+}
