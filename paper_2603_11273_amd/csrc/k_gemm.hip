@@ -1408,11 +1408,14 @@ void gemm_f32(const AView& a, const float* w, int M, int N, int K, const Epilogu
 // strip of 32 WN weight rows (output columns) and all 128 row slots over a K
 // range, in 64-deep chunks: each chunk's weight tile and activation tile go
 // global -> LDS with global_load_lds_dwordx4, eight lanes per 128-byte row
-// segment (whole cache lines per instruction), into an NS-stage ring with the
-// round-robin XOR swizzle of the encoder GEMM (16-byte slot c of row r holds
-// chunk c ^ ((r >> 1) & 7): conflict-free fragment reads).  Wave w computes
-// strip w % WN against 32 WN activation rows with v_mfma_f32_32x32x16_bf16:
-// weight rows are the "A" operand, activation rows the "B" operand.
+// segment (whole cache lines per instruction), with the round-robin XOR
+// swizzle of the encoder GEMM (16-byte slot c of row r holds chunk
+// c ^ ((r >> 1) & 7): conflict-free fragment reads).  The two operands have
+// rings of their own: the weights, which come cold from HBM, run NW chunks
+// ahead (most of a block's strip is in flight at once); the activations, an
+// L2 hit, run NX chunks ahead.  Wave w computes strip w % WN against 32 WN
+// activation rows with v_mfma_f32_32x32x16_bf16: weight rows are the "A"
+// operand, activation rows the "B" operand.
 constexpr int SK_BK = 64;          // K per chunk
 
 __device__ __forceinline__ int sk_swz(int row) { return (row >> 1) & 7; }
@@ -1433,27 +1436,49 @@ struct SkOut {
   float* logits;        // ARGMAX: optional float [D][N]
 };
 
-template <int WN, int NS, int EPI>
+// Loads issued after chunk c's activation tile (which follows every earlier
+// load in issue order): the prologue issues weight chunks 0 .. NW-2, then
+// activation chunks 0 .. NX-2; iteration c' issues weight chunk c' + NW - 1,
+// then activation chunk c' + NX - 1 (each only when it exists).
+template <int NW, int NX>
+__device__ __forceinline__ int sk_after(int c, int nck, int lpw, int lpx) {
+  int n = 0;
+  int first = c - NX + 2;                 // iterations that issued after X(c)
+  if (c <= NX - 2) {
+    n += lpx * max(0, min(NX - 2, nck - 1) - c);
+    first = 0;
+  }
+  for (int i = first; i < c; ++i)
+    n += (i + NW - 1 < nck ? lpw : 0) + (i + NX - 1 < nck ? lpx : 0);
+  return n;
+}
+
+template <int WN, int NW, int NX, int EPI>
 __global__ __launch_bounds__(256) void k_skinny_bf16(const bf16_t* __restrict__ x,
                                                      const bf16_t* __restrict__ w, int D, int N,
                                                      int K, int KC, SkOut o) {
   constexpr int RB = WN;                         // row blocks of 32 per wave
   constexpr int WR = 32 * WN;                    // weight rows per block
-  constexpr int STAGE = (WR + 128) * SK_BK;      // elements per ring stage
-  constexpr int LPC = 4 + WN;                    // DMA instructions per wave per chunk
+  constexpr int WSTAGE = WR * SK_BK, XSTAGE = 128 * SK_BK;   // elements per ring stage
+  constexpr int LPW = WN, LPX = 4;               // DMA instructions per wave per chunk
+  constexpr int MAXOUT = (NW - 1) * LPW + (NX - 1) * LPX;
+  static_assert(MAXOUT < 64, "vmcnt");
   extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
+  bf16_t* wring = smem;
+  bf16_t* xring = smem + NW * WSTAGE;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int l32 = lane & 31, lh = lane >> 5;
   const int n0 = blockIdx.x * WR, split = blockIdx.y;
   const int kb = split * KC, nck = KC / SK_BK;
   const uint32_t lds0 = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) bf16_t*)smem);
+  const uint32_t xlds0 = lds0 + (uint32_t)(NW * WSTAGE * 2);
   // DMA: instruction i of a wave fills rows 8 i .. 8 i + 7 of its share; lane
   // l lands at slot l % 8 of row l / 8 and fetches chunk (l % 8) ^ swz(row)
   uint32_t xdst[4], wdst[WN], xoff[4], woff[WN];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int row = wave * 32 + i * 8;                               // activation rows
-    xdst[i] = __builtin_amdgcn_readfirstlane(lds0 + (uint32_t)((WR + row) * SK_BK * 2));
+    xdst[i] = __builtin_amdgcn_readfirstlane(xlds0 + (uint32_t)(row * SK_BK * 2));
     const int r = row + (lane >> 3);
     xoff[i] = (uint32_t)(((int64_t)min(r, D - 1) * K + kb + (((lane & 7) ^ sk_swz(r)) * 8)) * 2);
   }
@@ -1464,14 +1489,17 @@ __global__ __launch_bounds__(256) void k_skinny_bf16(const bf16_t* __restrict__ 
     const int r = row + (lane >> 3);
     woff[i] = (uint32_t)(((int64_t)min(n0 + r, N - 1) * K + kb + (((lane & 7) ^ sk_swz(r)) * 8)) * 2);
   }
-  auto issue = [&](int c) {
-    const uint32_t so = (uint32_t)((c % NS) * STAGE * 2);
-    const bf16_t* xk = x + c * SK_BK;
+  auto issue_w = [&](int c) {
+    const uint32_t so = (uint32_t)((c % NW) * WSTAGE * 2);
     const bf16_t* wk = w + c * SK_BK;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) lds_dma16_s(xdst[i] + so, xoff[i], xk);
-#pragma unroll
     for (int i = 0; i < WN; ++i) lds_dma16_s(wdst[i] + so, woff[i], wk);
+  };
+  auto issue_x = [&](int c) {
+    const uint32_t so = (uint32_t)((c % NX) * XSTAGE * 2);
+    const bf16_t* xk = x + c * SK_BK;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) lds_dma16_s(xdst[i] + so, xoff[i], xk);
   };
   const int strip = wave % WN, rg = wave / WN;                      // this wave's strip, row group
   const int wrow = strip * 32 + l32, sww = sk_swz(wrow);
@@ -1487,25 +1515,26 @@ __global__ __launch_bounds__(256) void k_skinny_bf16(const bf16_t* __restrict__ 
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
 
-#pragma unroll
-  for (int c = 0; c < NS - 1; ++c)
-    if (c < nck) issue(c);
+  for (int c = 0; c < NW - 1 && c < nck; ++c) issue_w(c);
+  for (int c = 0; c < NX - 1 && c < nck; ++c) issue_x(c);
   for (int c = 0; c < nck; ++c) {
-    // this wave's loads of chunk c are done when at most the later issued
-    // chunks' loads are outstanding; the barrier then publishes every wave's
-    // share and frees the stage of chunk c - 1 for chunk c + NS - 1
-    wait_vmcnt_rt<LPC*(NS - 2)>(LPC * min(NS - 2, nck - 1 - c));
+    // this wave's tiles of chunk c have landed once at most the loads issued
+    // after them are outstanding; the barrier then publishes every wave's
+    // share and frees the stages of chunk c - 1 for the next issues
+    wait_vmcnt_rt<MAXOUT>(sk_after<NW, NX>(c, nck, LPW, LPX));
     __builtin_amdgcn_s_barrier();
-    if (c + NS - 1 < nck) issue(c + NS - 1);
-    const bf16_t* st = smem + (c % NS) * STAGE;
+    if (c + NW - 1 < nck) issue_w(c + NW - 1);
+    if (c + NX - 1 < nck) issue_x(c + NX - 1);
+    const bf16_t* wt = wring + (c % NW) * WSTAGE;
+    const bf16_t* xt = xring + (c % NX) * XSTAGE;
     bf16x8 wf[4], xf[4][RB];
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       const int ch = kk * 2 + lh;
-      wf[kk] = *(const bf16x8*)(st + wrow * SK_BK + ((ch ^ sww) * 8));
+      wf[kk] = *(const bf16x8*)(wt + wrow * SK_BK + ((ch ^ sww) * 8));
 #pragma unroll
       for (int j = 0; j < RB; ++j)
-        xf[kk][j] = *(const bf16x8*)(st + (WR + xrow[j]) * SK_BK + ((ch ^ swx[j]) * 8));
+        xf[kk][j] = *(const bf16x8*)(xt + xrow[j] * SK_BK + ((ch ^ swx[j]) * 8));
     }
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk)
@@ -1513,7 +1542,6 @@ __global__ __launch_bounds__(256) void k_skinny_bf16(const bf16_t* __restrict__ 
       for (int j = 0; j < RB; ++j)
         acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[kk], xf[kk][j], acc[j], 0, 0, 0);
   }
-
   // lane holds activation row xrow[j] and weight rows (output columns)
   // n0 + strip 32 + 8 (r / 4) + 4 (lane / 32) + r % 4
   const int nb = n0 + strip * 32;
@@ -1560,12 +1588,12 @@ __global__ __launch_bounds__(256) void k_skinny_bf16(const bf16_t* __restrict__ 
   }
 }
 
-template <int WN, int NS, int EPI>
+template <int WN, int NW, int NX, int EPI>
 static void launch_skinny(const bf16_t* x, const bf16_t* w, int D, int N, int K, int splits,
                           const SkOut& o, hipStream_t s) {
-  constexpr size_t lds = (size_t)NS * (32 * WN + 128) * SK_BK * sizeof(bf16_t);
+  constexpr size_t lds = ((size_t)NW * 32 * WN + (size_t)NX * 128) * SK_BK * sizeof(bf16_t);
   static_assert(lds <= 160 * 1024, "LDS");
-  auto kfn = k_skinny_bf16<WN, NS, EPI>;
+  auto kfn = k_skinny_bf16<WN, NW, NX, EPI>;
   static bool attr = false;
   if (!attr) {
     (void)hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -1591,17 +1619,16 @@ int dgemm_bf16(const bf16_t* x, const bf16_t* w, int D, int N, int K, int epi,
   // N % 32 == 0, K % 64 == 0 and D <= 128 are checked when the context is created
   if (D <= 0) return 1;
   SkOut o{out, bias, nullptr, nullptr};
-  // three stages (two 20-KB chunks in flight per block): deeper rings measure
-  // no faster at these sizes, where launch ramp-up and drain dominate
+  // weight ring 16 x 4 KB (15 chunks in flight), activation ring 3 x 16 KB
   if (epi == DG_PARTIAL) {
     const int sp = dgemm_splits(N, K);
-    launch_skinny<1, 3, SK_PARTIAL>(x, w, D, N, K, sp, o, s);
+    launch_skinny<1, 16, 3, SK_PARTIAL>(x, w, D, N, K, sp, o, s);
     return sp;
   }
   if (epi == DG_GELU)
-    launch_skinny<1, 3, SK_GELU>(x, w, D, N, K, 1, o, s);
+    launch_skinny<1, 16, 3, SK_GELU>(x, w, D, N, K, 1, o, s);
   else
-    launch_skinny<1, 3, SK_BIAS>(x, w, D, N, K, 1, o, s);
+    launch_skinny<1, 16, 3, SK_BIAS>(x, w, D, N, K, 1, o, s);
   return 1;
 }
 
@@ -1752,7 +1779,7 @@ void vocab_argmax_bf16(const bf16_t* x, const bf16_t* emb, int D, int V, int K, 
   if (D <= 0) return;
   (void)n_tiles;   // = vocab_tiles(V): the kernel derives it from V
   SkOut o{nullptr, nullptr, keys, logits};
-  launch_skinny<4, 4, SK_ARGMAX>(x, emb, D, V, K, 1, o, s);
+  launch_skinny<4, 6, 3, SK_ARGMAX>(x, emb, D, V, K, 1, o, s);
 }
 
 void vocab_logits_f32(const float* x, const float* emb, int D, int V, int K, float* logits,
