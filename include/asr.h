@@ -69,7 +69,7 @@ typedef enum { ASR_F32 = 0, ASR_BF16 = 1 } asr_dtype;
  * bfloat16 (round to nearest even) with float32 accumulation, float32
  * residual stream, LayerNorm and softmax; ASR_F32 keeps everything float32. */
 typedef struct {
-  int32_t n_mels;      /* 80 or 128 */
+  int32_t n_mels;      /* multiple of 8, at most 128 (Whisper: 80 or 128) */
   int32_t d_model;     /* multiple of 64 (of 128 for bf16), at most 2048 */
   int32_t n_enc;       /* encoder layers (>= 0) */
   int32_t n_dec;       /* decoder layers (>= 0) */

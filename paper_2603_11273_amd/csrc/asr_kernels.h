@@ -157,8 +157,8 @@ struct MelTables {
   const float* window;     // [400] periodic Hann
   const float* cos_t;      // [400] cos(2 pi j / 400)
   const float* sin_t;      // [400] sin(2 pi j / 400)
-  const float* fb;         // [n_mels][201] filterbank
-  const int32_t* fb_range; // [n_mels][2] first bin, bin count
+  const float* fb;         // packed nonzero filter weights, filter after filter (<= 402)
+  const int32_t* fb_range; // [n_mels][3] first bin, bin count, offset into fb
 };
 void log_mel(const float* const* pcm_ptrs, const int64_t* n_samples, int n_clips, int n_mels,
              const MelTables& t, float* mel_raw, uint32_t* clip_max, hipStream_t s);

@@ -278,7 +278,7 @@ void plan(asr_ctx* c) {
   L.cos_t = b.take(kNFFT * f4);
   L.sin_t = b.take(kNFFT * f4);
   L.fb = b.take(M * kBins * f4);
-  L.fb_range = b.take(M * 2 * 4);
+  L.fb_range = b.take(M * 3 * 4);
   L.sinus = b.take((int64_t)kCtx * d * f4);
   // per-slot caches [slot][n_dec][2][H][ctx][64]
   const int64_t S = g.max_slots;
@@ -358,7 +358,9 @@ double slaney_hz(double m) {
 }
 
 // Window, twiddles, mel filterbank (Slaney scale, area-normalised triangles
-// over the 201 bins) and each filter's nonzero bin range.
+// over the 201 bins) packed as each filter's nonzero bin range, filter after
+// filter, with [first bin, bin count, offset into the packed weights] per
+// filter (at most 2 x 201 weights: a bin lies under at most two triangles).
 struct HostMelTables {
   std::vector<float> win, ct, st, fb;
   std::vector<int32_t> rng;
@@ -375,8 +377,8 @@ HostMelTables host_mel_tables(int M) {
     t.ct[i] = (float)std::cos(a);
     t.st[i] = (float)std::sin(a);
   }
-  t.fb.assign((size_t)M * kBins, 0.f);
-  t.rng.assign((size_t)M * 2, 0);
+  std::vector<float> dense((size_t)M * kBins, 0.f);
+  t.rng.assign((size_t)M * 3, 0);
   std::vector<double> edge(M + 2);
   double mlo = slaney_mel(0.0), mhi = slaney_mel(kSampleRate / 2.0);
   for (int i = 0; i < M + 2; ++i) edge[i] = slaney_hz(mlo + (mhi - mlo) * i / (M + 1));
@@ -388,14 +390,20 @@ HostMelTables host_mel_tables(int M) {
       double up = (f - edge[m]) / (edge[m + 1] - edge[m]);
       double down = (edge[m + 2] - f) / (edge[m + 2] - edge[m + 1]);
       double w = std::max(0.0, std::min(up, down)) * norm;
-      t.fb[(size_t)m * kBins + k] = (float)w;
+      dense[(size_t)m * kBins + k] = (float)w;
       if (w > 0) {
         if (first < 0) first = k;
         last = k;
       }
     }
-    t.rng[2 * m] = first < 0 ? 0 : first;
-    t.rng[2 * m + 1] = first < 0 ? 0 : last - first + 1;
+    t.rng[3 * m] = first < 0 ? 0 : first;
+    t.rng[3 * m + 1] = first < 0 ? 0 : last - first + 1;
+  }
+  // packed nonzero range of every filter, filter after filter
+  for (int m = 0; m < M; ++m) {
+    t.rng[3 * m + 2] = (int32_t)t.fb.size();
+    for (int i = 0; i < t.rng[3 * m + 1]; ++i)
+      t.fb.push_back(dense[(size_t)m * kBins + t.rng[3 * m] + i]);
   }
   return t;
 }
@@ -954,7 +962,8 @@ asr_status asr_create(const asr_model_cfg* cfg, int32_t device, asr_ctx** out) {
   const asr_model_cfg& g = *cfg;
   if (g.n_mels <= 0 || g.d_model <= 0 || g.n_head <= 0 || g.d_model != 64 * g.n_head)
     return fail(ASR_EINVAL, "d_model must equal 64 * n_head");
-  if (g.n_mels % 8 != 0) return fail(ASR_EINVAL, "n_mels must be a multiple of 8");
+  if (g.n_mels % 8 != 0 || g.n_mels > 128)
+    return fail(ASR_EINVAL, "n_mels must be a multiple of 8, at most 128");
   if (g.d_model > 2048) return fail(ASR_EINVAL, "d_model must be <= 2048");
   if (g.d_ffn <= 0 || g.d_ffn % 64 != 0) return fail(ASR_EINVAL, "d_ffn must be a multiple of 64");
   if (g.dtype == ASR_BF16 && (g.d_model % 128 != 0 || g.d_ffn % 128 != 0))
@@ -1878,8 +1887,8 @@ constexpr int kNaDevices = 64;
 // word offsets into the scratch array
 constexpr size_t kNaWin = 0, kNaCos = kNaWin + kNFFT, kNaSin = kNaCos + kNFFT;
 constexpr size_t kNaFb80 = kNaSin + kNFFT, kNaFb128 = kNaFb80 + (size_t)80 * kBins;
-constexpr size_t kNaRng80 = kNaFb128 + (size_t)128 * kBins, kNaRng128 = kNaRng80 + 2 * 80;
-constexpr size_t kNaMax = kNaRng128 + 2 * 128;
+constexpr size_t kNaRng80 = kNaFb128 + (size_t)128 * kBins, kNaRng128 = kNaRng80 + 3 * 80;
+constexpr size_t kNaMax = kNaRng128 + 3 * 128;
 constexpr size_t kNaWords = kNaMax + kMelArgClips;
 constexpr size_t kNaBytes = 192 * 1024;   // the stated maximum: 192 KiB per GPU
 static_assert(kNaWords * 4 <= kNaBytes, "scratch layout");

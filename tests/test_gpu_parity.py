@@ -21,7 +21,9 @@ def _clips(seed, lengths):
 # ----------------------------------------------------------------------------
 # log-mel front-end
 # ----------------------------------------------------------------------------
-@pytest.mark.parametrize("n_mels", [80, 128])
+# 80 and 128 are Whisper's; 16 and 40 have filters wider than 16 bins, which
+# take the kernel's path for bins past the first 16
+@pytest.mark.parametrize("n_mels", [16, 40, 80, 128])
 def test_logmel_matches_oracle(n_mels):
     from paper_2603_11273_amd import asr
     shape = synth.ModelShape("mel", n_mels, 384, 1, 0, 6, 1536, 0, "f32")
