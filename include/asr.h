@@ -380,7 +380,7 @@ asr_status asr_debug_set_self_kv(asr_ctx* ctx, int32_t slot, const float* src, i
  * For callers that cannot allocate device memory or bind a workspace (code
  * under HIP graph capture, tight serving loops, harnesses that forbid
  * hipMalloc): the log-mel front-end of asr_debug_logmel with its scratch in
- * a file-scope device array of the library (192 KiB per GPU, held until the
+ * a file-scope device array of the library (64 KiB per GPU, held until the
  * process ends) instead of a bound block.  Needs no context.
  *   pcm[i]: device pointer to clip i's float32 samples (n_samples[i] in
  *   [0, 480000]; may be NULL when 0); pcm and n_samples are host arrays of n
@@ -392,8 +392,9 @@ asr_status asr_debug_set_self_kv(asr_ctx* ctx, int32_t slot, const float* src, i
  * arguments.  The first call on a device resolves the array's address and
  * uploads the constant tables with synchronous copies, so a caller that
  * captures graphs makes one call before capturing.  All calls on one GPU
- * share its array (the per-clip maxima are cleared at the start of every
- * call): calls that overlap on one GPU race.
+ * share its array (every call writes all the per-group maxima it reads, so
+ * nothing carries over from an earlier call): calls that overlap on one GPU
+ * race.
  * Errors: EINVAL (NULL argument, n or n_mels out of range, n_samples out of
  * range), EDEVICE (HIP error). */
 asr_status asr_logmel_noalloc(const float* const* pcm, const int64_t* n_samples, int32_t n,

@@ -31,11 +31,19 @@ template <>
 struct St<float> {
   static __device__ __forceinline__ float ld(const float* p, int64_t i) { return p[i]; }
   static __device__ __forceinline__ void st(float* p, int64_t i, float v) { p[i] = v; }
+  // four values at element i (i a multiple of 4, p 16-byte aligned)
+  static __device__ __forceinline__ void st4(float* p, int64_t i, float4 v) {
+    *(float4*)(p + i) = v;
+  }
 };
 template <>
 struct St<bf16_t> {
   static __device__ __forceinline__ float ld(const bf16_t* p, int64_t i) { return bf2f(p[i]); }
   static __device__ __forceinline__ void st(bf16_t* p, int64_t i, float v) { p[i] = f2bf(v); }
+  // four values at element i (i a multiple of 4, p 8-byte aligned)
+  static __device__ __forceinline__ void st4(bf16_t* p, int64_t i, float4 v) {
+    *(uint2*)(p + i) = make_uint2(pack2_bf16(v.x, v.y), pack2_bf16(v.z, v.w));
+  }
 };
 
 // GELU(x) = x Phi(x), Phi the standard normal CDF, with erf from

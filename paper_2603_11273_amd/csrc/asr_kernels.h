@@ -160,8 +160,13 @@ struct MelTables {
   const float* fb;         // packed nonzero filter weights, filter after filter (<= 402)
   const int32_t* fb_range; // [n_mels][3] first bin, bin count, offset into fb
 };
+// The front-end transforms kMelGroupFrames consecutive frames of a clip at a
+// time and stores each group's largest log-mel value in group_max
+// [n_clips][kMelGroups]; mel_normalize reduces a clip's groups to its maximum.
+constexpr int kMelGroupFrames = 16;
+constexpr int kMelGroups = (kFrames + kMelGroupFrames - 1) / kMelGroupFrames;   // 188
 void log_mel(const float* const* pcm_ptrs, const int64_t* n_samples, int n_clips, int n_mels,
-             const MelTables& t, float* mel_raw, uint32_t* clip_max, hipStream_t s);
+             const MelTables& t, float* mel_raw, float* group_max, hipStream_t s);
 // The same with the clips' pointers and lengths in the kernel arguments (no
 // device-side lists), for up to kMelArgClips clips.
 constexpr int kMelArgClips = 64;
@@ -170,9 +175,9 @@ struct MelClipArgs {
   int64_t n[kMelArgClips];
 };
 void log_mel_args(const MelClipArgs& clips, int n_clips, int n_mels, const MelTables& t,
-                  float* mel_raw, uint32_t* clip_max, hipStream_t s);
+                  float* mel_raw, float* group_max, hipStream_t s);
 template <typename T>
-void mel_normalize(const float* mel_raw, const uint32_t* clip_max, int n_clips, int n_mels,
+void mel_normalize(const float* mel_raw, const float* group_max, int n_clips, int n_mels,
                    T* out, int pad_rows, hipStream_t s);
 
 // Utility kernels.

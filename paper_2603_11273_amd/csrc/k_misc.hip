@@ -274,19 +274,26 @@ template void embed<bf16_t>(const bf16_t*, const float*, const int32_t*, const i
 // frame's 400-point DFT of the windowed samples as a mixed-radix FFT,
 // 400 = 16 x 25 (Cooley-Tukey with n = 25 n1 + n2, k = k1 + 16 k2):
 //   1. for every n2, the 16-point DFT over n1 of the real sequence
-//      y[25 n1 + n2] (bins 0 .. 8 by folding y[n1] +- y[16 - n1]; bins
-//      9 .. 15 are the conjugates of bins 7 .. 1), times the twiddle
-//      e^{-2 pi i k1 n2 / 400};
-//   2. for every k1, the 25-point DFT over n2, itself 5 x 5 (two passes of
-//      5-point butterflies with the e^{-2 pi i j1 m2 / 25} twiddles between);
-// bins k = k1 + 16 k2 <= 200 give the power spectrum.  The block then
-// applies the mel filters (each filter's nonzero bin range only), takes
-// log10 with the 1e-10 floor, and folds its maximum into the clip's maximum
-// with an atomic max on order-preserving integer keys.
+//      y[25 n1 + n2], bins k1 = 0 .. 8 (folding y[n1] +- y[16 - n1]), times
+//      the twiddle e^{-2 pi i k1 n2 / 400};
+//   2. for k1 = 0 .. 8, the 25-point DFT over n2, itself 5 x 5 (two passes of
+//      5-point butterflies with the e^{-2 pi i j1 m2 / 25} twiddles between).
+// The input is real, so X[400 - k] = conj X[k]: bin (16 - k1) + 16 k2 is
+// the conjugate of bin k1 + 16 (24 - k2), and columns k1 = 0 .. 8 give every
+// bin's power -- column k1 writes bin k when k <= 200, else bin 400 - k
+// (columns 0 and 8 are their own mirror images and write k <= 200 only).
+// The block then applies the mel filters (each filter's nonzero bin range
+// only), takes log10 with the 1e-10 floor, and stores the group's maximum
+// (a plain store per group: the normalisation reduces a clip's groups, so
+// there is no atomic for the blocks working on one clip to queue on).
 // ---------------------------------------------------------------------------
-constexpr int MEL_FR = 16;
+constexpr int MEL_FR = kMelGroupFrames;
 constexpr int MEL_SEG = (MEL_FR - 1) * kHop + kNFFT;   // 2800 samples
-constexpr int MEL_BLD = 17;                            // padded row (float2) of stage-1 output
+constexpr int MEL_COLS = 9;                            // stage-1 bins k1 = 0 .. 8
+// float2 stride of one frame's stage-1 output [25][MEL_COLS], padded to 9
+// mod 32 so that stage 2's lanes (frame, k1) = (t / 9, t % 9) read 32
+// consecutive words per half-wave
+constexpr int MEL_FST = 25 * MEL_COLS + 8;
 
 // Where a clip's samples are: device arrays of pointers and lengths, or the
 // same lists carried in the kernel arguments (MelClipArgs).
@@ -331,41 +338,54 @@ __device__ __forceinline__ void dft5(float* ar, float* ai) {
 // groups persistently (group g, g + gridDim.x, ...), and while one group is
 // transformed the samples of the block's next group are already loading into
 // registers (MEL_PT per thread), so the global latency hides behind the FFT.
-constexpr int MEL_GROUPS = (kFrames + MEL_FR - 1) / MEL_FR;   // groups per clip
+constexpr int MEL_GROUPS = kMelGroups;                         // groups per clip
+// clips per launch: their pointers and lengths sit in LDS, read there by
+// every group (LDS waits are independent of the loads and stores in flight)
+constexpr int MEL_LAUNCH_CLIPS = 256;
 constexpr int MEL_PT = (MEL_SEG + 255) / 256;                // samples per thread
 
 template <class Clips>
 __global__ __launch_bounds__(256) void k_log_mel(Clips clips, int n_clips, int n_mels,
                                                  MelTables tb, float* mel_raw,
-                                                 uint32_t* clip_max) {
-  // the samples are dead once stage 1 has read them: the power spectrum
-  // [MEL_FR][kBins + 3] reuses their LDS (16 floats of slack: a filter's
-  // 16-bin window may start at bin 200 of the last row)
-  constexpr int SEGPW = (MEL_SEG > MEL_FR * (kBins + 3) ? MEL_SEG : MEL_FR * (kBins + 3)) + 16;
-  __shared__ float segpw[SEGPW];
-  __shared__ float2 bst[MEL_FR * 25 * MEL_BLD];          // stage-1 output [f][n2][k1]
+                                                 float* group_max) {
+  // segment samples and the power spectrum [MEL_FR][kBins + 3] (16 floats
+  // of slack: a filter's bin window may run past the last row's bin 200)
+  constexpr int SEG_SLOTS = MEL_PT * 256;
+  __shared__ float seg[SEG_SLOTS];
+  __shared__ float pwbuf[MEL_FR * (kBins + 3) + 16];
+  __shared__ float2 bst[MEL_FR * MEL_FST];               // stage-1 output [f][n2][k1]
   __shared__ float fbw[2 * kBins];                       // packed filter weights (bins past 16)
   __shared__ float red[4];
-  float* seg = segpw;
-  float (*pw)[kBins + 3] = (float (*)[kBins + 3])segpw;
+  __shared__ const float* c_ptr[MEL_LAUNCH_CLIPS];
+  __shared__ int32_t c_len[MEL_LAUNCH_CLIPS];             // samples used: at most 30 s
+  float (*pw)[kBins + 3] = (float (*)[kBins + 3])pwbuf;
   const int tid = threadIdx.x;
   const int n_items = n_clips * MEL_GROUPS;
 
+  // the power spectrum's padding (bins 201 .. 203 of every row and the
+  // slack after the last) is never written by stage 2 and stays zero, so
+  // a filter's reads past its own bins multiply a finite value (or zero) by
+  // its zero weights, as the dense filterbank product would
+  for (int i = tid; i < MEL_FR * (kBins + 3) + 16; i += 256) pwbuf[i] = 0.0f;
+  for (int i = tid; i < n_clips; i += 256) {
+    const int64_t n = clips.len(i);
+    c_ptr[i] = n > 0 ? clips.ptr(i) : tb.window;   // a clip without samples reads the window
+    c_len[i] = (int32_t)(n < kSamples30s ? n : kSamples30s);
+  }
   // Every table a thread uses depends only on its fixed role, so it sits in
   // registers for the whole kernel instead of being re-read from LDS.
   // Stage-1 role: n2 = tid % 25 for frames tid / 25 and tid / 25 + 10
   // (threads 250 .. 255 idle); the window samples w[25 n1 + n2] and the
-  // twiddles e^{-2 pi i k n2 / 400} of bins k1 = 1 .. 8 and 16 - k1.
+  // twiddles e^{-2 pi i k1 n2 / 400} of bins k1 = 1 .. 8.
   const int s1_n2 = tid % 25, s1_fs = tid / 25;
   const bool s1_on = tid < 250;
-  float s1_win[16], tw_c[16], tw_s[16];
+  float s1_win[16], tw_c[MEL_COLS], tw_s[MEL_COLS];
 #pragma unroll
   for (int n1 = 0; n1 < 16; ++n1) s1_win[n1] = tb.window[25 * n1 + s1_n2];
 #pragma unroll
-  for (int k1 = 1; k1 < 16; ++k1) {
-    const int t = k1 * s1_n2 % kNFFT;
-    tw_c[k1] = tb.cos_t[t];
-    tw_s[k1] = tb.sin_t[t];
+  for (int k1 = 1; k1 < MEL_COLS; ++k1) {
+    tw_c[k1] = tb.cos_t[k1 * s1_n2];   // k1 n2 < 400
+    tw_s[k1] = tb.sin_t[k1 * s1_n2];
   }
   // Mel role: filter m = tid % n_mels for frames tid / n_mels + j * mel_fs
   // (threads past mel_fs * n_mels idle), with the filter's first 16 weights
@@ -387,31 +407,48 @@ __global__ __launch_bounds__(256) void k_log_mel(Clips clips, int n_clips, int n
     const int nw = tb.fb_range[3 * (n_mels - 1) + 2] + tb.fb_range[3 * (n_mels - 1) + 1];
     for (int i = tid; i < nw; i += 256) fbw[i] = tb.fb[i];   // <= 2 x 201
   }
+  // Land the table loads here, once: their first uses sit in branches
+  // inside the group loop, where the compiler's wait analysis cannot see
+  // that they completed and would otherwise wait for every load and store
+  // in flight at each of them.
+#pragma unroll
+  for (int i = 0; i < 16; ++i) asm volatile("" : "+v"(s1_win[i]), "+v"(m_w[i]));
+#pragma unroll
+  for (int i = 1; i < MEL_COLS; ++i) asm volatile("" : "+v"(tw_c[i]), "+v"(tw_s[i]));
 
-  // sample index (reflect padding at both ends of the 30-s segment) of slot
-  // u of group `it`'s segment; slots past MEL_SEG (the last 16 of 256 MEL_PT)
-  // map to valid samples too and land in LDS beyond the segment, unread
-  auto sample_index = [&](int f0, int u) {
-    int64_t sidx = (int64_t)f0 * kHop - kNFFT / 2 + tid + u * 256;
+  // Group `it`'s segment starts at sample f0 * kHop - kNFFT / 2 of its clip;
+  // it is interior when it needs neither reflection nor zeros (all of it
+  // inside the clip's own samples), the common case, which takes plain
+  // loads at constant offsets.  Slot u of thread tid is segment sample
+  // tid + 256 u; slots past MEL_SEG (the last 16 of 256 MEL_PT) are valid
+  // samples too and land in LDS beyond the segment, unread.
+  auto seg_start = [&](int f0) { return f0 * kHop - kNFFT / 2; };
+  auto interior = [&](int start, int n) { return start >= 0 && start + MEL_PT * 256 <= n; };
+  // sample index of slot u at a segment edge (reflect padding at both ends
+  // of the 30-s segment)
+  auto edge_index = [&](int start, int u) {
+    int sidx = start + tid + u * 256;
     if (sidx < 0) sidx = -sidx;
-    if (sidx >= kSamples30s) sidx = 2 * (int64_t)(kSamples30s - 1) - sidx;
+    if (sidx >= kSamples30s) sidx = 2 * (kSamples30s - 1) - sidx;
     return sidx;
   };
-  // samples of group `it` into registers.  Every load is unconditional (the
-  // index is clamped into the clip, and a clip without samples reads the
-  // window table instead) and the zeros past the clip's own samples are a
-  // select at use, so all MEL_PT loads are in flight at once rather than
-  // each waited on in its own branch.
+  // samples of group `it` into registers.  Every load is unconditional (at
+  // an edge the index is clamped into the clip's samples; the zeros past
+  // them are a select at use), so all MEL_PT loads are in flight at once
+  // rather than each waited on in its own branch.
   auto fetch = [&](int it, float (&r)[MEL_PT]) {
     const int clip = it / MEL_GROUPS, f0 = (it - clip * MEL_GROUPS) * MEL_FR;
-    const int64_t n = clips.len(clip);
+    const int n = c_len[clip];
     typedef const __attribute__((address_space(1))) float* gptr;   // global memory
-    const gptr x = (gptr)(n > 0 ? clips.ptr(clip) : tb.window);
-    const int64_t last = n > 0 ? n - 1 : 0;
+    const gptr x = (gptr)c_ptr[clip];
+    const int start = seg_start(f0);
+    if (interior(start, n)) {
 #pragma unroll
-    for (int u = 0; u < MEL_PT; ++u) {
-      const int64_t sidx = sample_index(f0, u);
-      r[u] = x[sidx < last ? sidx : last];
+      for (int u = 0; u < MEL_PT; ++u) r[u] = x[start + tid + u * 256];
+    } else {
+      const int last = n > 0 ? n - 1 : 0;
+#pragma unroll
+      for (int u = 0; u < MEL_PT; ++u) r[u] = x[min(edge_index(start, u), last)];
     }
   };
   // stage 1 for frame f of the group: the 16-point DFT over n1 of the
@@ -426,9 +463,9 @@ __global__ __launch_bounds__(256) void k_log_mel(Clips clips, int n_clips, int n
       sp[m] = y[m] + y[16 - m];
       dm[m] = y[m] - y[16 - m];
     }
-    float2* row = bst + (f * 25 + s1_n2) * MEL_BLD;
+    float2* row = bst + f * MEL_FST + s1_n2 * MEL_COLS;
 #pragma unroll
-    for (int k1 = 0; k1 <= 8; ++k1) {
+    for (int k1 = 0; k1 < MEL_COLS; ++k1) {
       float re = y[0] + ((k1 & 1) ? -y[8] : y[8]), im = 0.f;
 #pragma unroll
       for (int m = 1; m < 8; ++m) {
@@ -436,31 +473,36 @@ __global__ __launch_bounds__(256) void k_log_mel(Clips clips, int n_clips, int n
         re = fmaf(sp[m], kC16[j], re);
         im = fmaf(-dm[m], kS16[j], im);
       }
-      if (k1 == 0) {
-        row[0] = make_float2(re, im);
-      } else {
-        // twiddle e^{-2 pi i k1 n2 / 400} on bin k1 and (conjugate input) on bin 16 - k1
-        row[k1] = make_float2(re * tw_c[k1] + im * tw_s[k1], im * tw_c[k1] - re * tw_s[k1]);
-        if (k1 <= 7) {                        // conj(A) = (re, -im)
-          const int k2 = 16 - k1;
-          row[k2] = make_float2(re * tw_c[k2] - im * tw_s[k2], -im * tw_c[k2] - re * tw_s[k2]);
-        }
-      }
+      // twiddle e^{-2 pi i k1 n2 / 400}
+      row[k1] = k1 == 0 ? make_float2(re, im)
+                        : make_float2(re * tw_c[k1] + im * tw_s[k1], im * tw_c[k1] - re * tw_s[k1]);
     }
   };
-  // one group: its samples (in `cur`) into LDS, the next group's samples
-  // into `nxt`, then the transform and the filterbank
-  auto process = [&](int it, const float (&cur)[MEL_PT], float (&nxt)[MEL_PT]) {
+  // the samples of a group from registers into LDS (zeros past the clip's
+  // own samples)
+  auto put = [&](int it, const float (&r)[MEL_PT]) {
     const int clip = it / MEL_GROUPS, f0 = (it - clip * MEL_GROUPS) * MEL_FR;
-    __syncthreads();                         // the previous group is done with the LDS
-    static_assert(MEL_PT * 256 <= SEGPW, "segment slots");
-    {
-      const int64_t n = clips.len(clip);
+    const int n = c_len[clip];
+    const int start = seg_start(f0);
+    if (interior(start, n)) {
 #pragma unroll
-      for (int u = 0; u < MEL_PT; ++u) seg[tid + u * 256] = sample_index(f0, u) < n ? cur[u] : 0.0f;
+      for (int u = 0; u < MEL_PT; ++u) seg[tid + u * 256] = r[u];
+    } else {
+#pragma unroll
+      for (int u = 0; u < MEL_PT; ++u) seg[tid + u * 256] = edge_index(start, u) < n ? r[u] : 0.0f;
     }
-    if (it + (int)gridDim.x < n_items) fetch(it + gridDim.x, nxt);
-    __syncthreads();
+  };
+  // One group, its samples already in LDS.  The next group's samples load
+  // into registers at the start and go to LDS after stage 2 (the segment is
+  // free once stage 1 is done), so their latency hides behind two stages
+  // and the wait for them comes before this group's stores are issued.
+  // Three barriers: stage-1 output ready (segment free), power spectrum and
+  // next segment ready, wave maxima ready.
+  float nxt[MEL_PT];
+  auto process = [&](int it) {
+    const int clip = it / MEL_GROUPS, f0 = (it - clip * MEL_GROUPS) * MEL_FR;
+    const int it_next = it + (int)gridDim.x;
+    if (it_next < n_items) fetch(it_next, nxt);
 
     if (s1_on) {
       stage1(s1_fs);
@@ -468,16 +510,17 @@ __global__ __launch_bounds__(256) void k_log_mel(Clips clips, int n_clips, int n
     }
     __syncthreads();
 
-    // stage 2: (frame f, k1) -> 25 bins over n2 = 5 m1 + m2, as 5 x 5
-    {
-      const int f = tid >> 4, k1 = tid & 15;
+    // stage 2: (frame f, k1 <= 8) -> 25 bins over n2 = 5 m1 + m2, as 5 x 5
+    if (tid < MEL_FR * MEL_COLS) {
+      const int f = tid / MEL_COLS, k1 = tid - f * MEL_COLS;
+      const float2* col = bst + f * MEL_FST + k1;
       float cr[5][5], ci[5][5];               // [m2][j1]
 #pragma unroll
       for (int m2 = 0; m2 < 5; ++m2) {
         float ar[5], ai[5];
 #pragma unroll
         for (int m1 = 0; m1 < 5; ++m1) {
-          const float2 v = bst[(f * 25 + 5 * m1 + m2) * MEL_BLD + k1];
+          const float2 v = col[(5 * m1 + m2) * MEL_COLS];
           ar[m1] = v.x;
           ai[m1] = v.y;
         }
@@ -490,6 +533,7 @@ __global__ __launch_bounds__(256) void k_log_mel(Clips clips, int n_clips, int n
           ci[m2][j1] = ai[j1] * c - ar[j1] * sn;
         }
       }
+      const bool mirror = k1 >= 1 && k1 <= 7;
 #pragma unroll
       for (int j1 = 0; j1 < 5; ++j1) {
         float ar[5], ai[5];
@@ -502,16 +546,20 @@ __global__ __launch_bounds__(256) void k_log_mel(Clips clips, int n_clips, int n
 #pragma unroll
         for (int j2 = 0; j2 < 5; ++j2) {
           const int k = k1 + 16 * (j1 + 5 * j2);
-          if (k < kBins) pw[f][k] = ar[j2] * ar[j2] + ai[j2] * ai[j2];
+          const float p = ar[j2] * ar[j2] + ai[j2] * ai[j2];
+          if (k < kBins) pw[f][k] = p;
+          else if (mirror) pw[f][kNFFT - k] = p;
         }
       }
     }
+    if (it_next < n_items) put(it_next, nxt);
     __syncthreads();
 
     // filterbank, log10 with the 1e-10 floor, the group's maximum; each
     // frame reads NB bins from the filter's first, NB the widest filter of
     // the wave rounded up (one straight-line variant per width)
     float local_max = -INFINITY;
+    float* const out_g = mel_raw + ((int64_t)clip * kFrames + f0 + m_f) * n_mels + mm;
     auto filters = [&](auto nb) {
       constexpr int NB = decltype(nb)::value;
 #pragma unroll
@@ -522,42 +570,38 @@ __global__ __launch_bounds__(256) void k_log_mel(Clips clips, int n_clips, int n
         float v[NB];
 #pragma unroll
         for (int i = 0; i < NB; ++i) v[i] = prow[i];
-        // bins past the lane's own filter carry zero weight; the select
-        // keeps whatever they hold out of the sum
+        // bins past the lane's own filter carry zero weight
         float acc = 0.f;
 #pragma unroll
-        for (int i = 0; i < NB; ++i) acc = fmaf(m_w[i], i < m_cnt ? v[i] : 0.0f, acc);
+        for (int i = 0; i < NB; ++i) acc = fmaf(m_w[i], v[i], acc);
         for (int i = 16; i < m_cnt; ++i) acc = fmaf(fbw[m_off + i], prow[i], acc);
-        const float L = log10f(fmaxf(acc, 1e-10f));
-        mel_raw[((int64_t)clip * kFrames + f0 + f) * n_mels + mm] = L;
+        // log10 as log2 times log10(2) (the argument is a normal float)
+        const float L = __builtin_amdgcn_logf(fmaxf(acc, 1e-10f)) * 0.30102999566398120f;
+        out_g[(int64_t)j * mel_fs * n_mels] = L;
         local_max = fmaxf(local_max, L);
       }
     };
     if (wave_cnt <= 2) filters(std::integral_constant<int, 2>());
     else if (wave_cnt <= 4) filters(std::integral_constant<int, 4>());
+    else if (wave_cnt <= 6) filters(std::integral_constant<int, 6>());
     else if (wave_cnt <= 8) filters(std::integral_constant<int, 8>());
+    else if (wave_cnt <= 10) filters(std::integral_constant<int, 10>());
     else if (wave_cnt <= 12) filters(std::integral_constant<int, 12>());
+    else if (wave_cnt <= 14) filters(std::integral_constant<int, 14>());
     else filters(std::integral_constant<int, 16>());
     local_max = wave_max(local_max);
     if ((tid & 63) == 0) red[tid >> 6] = local_max;
     __syncthreads();
-    if (tid == 0) {
-      float mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-      atomicMax(clip_max + clip, ordered_u32(mx));
-    }
+    if (tid == 0) group_max[it] = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   };
-  // ping-pong between two register sets, so no copy forces the next group's
-  // loads to land before this group's work
-  float sa[MEL_PT], sb[MEL_PT];
+  __syncthreads();                           // clip lists in LDS
   int it = blockIdx.x;
-  if (it < n_items) fetch(it, sa);
-  while (it < n_items) {
-    process(it, sa, sb);
-    it += gridDim.x;
-    if (it >= n_items) break;
-    process(it, sb, sa);
-    it += gridDim.x;
+  if (it < n_items) {
+    fetch(it, nxt);
+    put(it, nxt);
   }
+  __syncthreads();
+  for (; it < n_items; it += gridDim.x) process(__builtin_amdgcn_readfirstlane(it));
 }
 
 // Resident blocks of the log-mel kernel (two per CU with its LDS).
@@ -575,55 +619,86 @@ static int mel_grid(int n_clips) {
 }
 
 void log_mel(const float* const* pcm_ptrs, const int64_t* n_samples, int n_clips, int n_mels,
-             const MelTables& t, float* mel_raw, uint32_t* clip_max, hipStream_t s) {
+             const MelTables& t, float* mel_raw, float* group_max, hipStream_t s) {
   if (n_clips <= 0 || n_mels <= 0 || n_mels > 128) return;   // the kernel's LDS holds 128 filters
-  fill_u32(clip_max, 0u, n_clips, s);
-  k_log_mel<ClipsInMemory><<<mel_grid<ClipsInMemory>(n_clips), 256, 0, s>>>(
-      ClipsInMemory{pcm_ptrs, n_samples}, n_clips, n_mels, t, mel_raw, clip_max);
+  for (int c0 = 0; c0 < n_clips; c0 += MEL_LAUNCH_CLIPS) {
+    const int nc = std::min(MEL_LAUNCH_CLIPS, n_clips - c0);
+    k_log_mel<ClipsInMemory><<<mel_grid<ClipsInMemory>(nc), 256, 0, s>>>(
+        ClipsInMemory{pcm_ptrs + c0, n_samples + c0}, nc, n_mels, t,
+        mel_raw + (size_t)c0 * kFrames * n_mels, group_max + (size_t)c0 * MEL_GROUPS);
+  }
 }
 
 void log_mel_args(const MelClipArgs& clips, int n_clips, int n_mels, const MelTables& t,
-                  float* mel_raw, uint32_t* clip_max, hipStream_t s) {
-  if (n_clips <= 0 || n_mels <= 0 || n_mels > 128) return;
-  fill_u32(clip_max, 0u, n_clips, s);
+                  float* mel_raw, float* group_max, hipStream_t s) {
+  static_assert(kMelArgClips <= MEL_LAUNCH_CLIPS, "one launch");
+  if (n_clips <= 0 || n_clips > kMelArgClips || n_mels <= 0 || n_mels > 128) return;
   k_log_mel<ClipsInArgs><<<mel_grid<ClipsInArgs>(n_clips), 256, 0, s>>>(
-      ClipsInArgs{clips}, n_clips, n_mels, t, mel_raw, clip_max);
+      ClipsInArgs{clips}, n_clips, n_mels, t, mel_raw, group_max);
 }
 
 // Dynamic-range clamp 8 below the clip's maximum, then (x + 4) / 4.  With
 // pad_rows = 1 the output has a zero row before and after each clip's 3000
-// frames, which the first stem convolution reads as its zero padding.
-template <typename T>
-__global__ void k_mel_norm(const float* mel_raw, const uint32_t* clip_max, int n_mels, T* out,
-                           int pad_rows) {
-  int clip = blockIdx.y;
-  int rows_out = kFrames + 2 * pad_rows;
-  float floor_v = from_ordered_u32(clip_max[clip]) - 8.0f;
-  int64_t n = (int64_t)rows_out * n_mels;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    int64_t r = i / n_mels;
-    int m = (int)(i - r * n_mels);
-    int64_t frame = r - pad_rows;
-    float v = 0.f;
-    if (frame >= 0 && frame < kFrames) {
-      float L = mel_raw[((int64_t)clip * kFrames + frame) * n_mels + m];
-      v = (fmaxf(L, floor_v) + 4.0f) * 0.25f;
+// frames, which the first stem convolution reads as its zero padding.  Rows
+// are contiguous in both layouts, so output element i of a clip is input
+// element i - pad_rows * n_mels (zero outside the frames): V at a time (V =
+// 4 when both buffers are aligned for it; n_mels is a multiple of 8).  The
+// clip's maximum is the largest of its groups' maxima, reduced by the first
+// wave of each block.
+template <typename T, int V>
+__global__ __launch_bounds__(256) void k_mel_norm(const float* mel_raw, const float* group_max,
+                                                  int n_mels, T* out, int pad_rows) {
+  __shared__ float s_floor;
+  const int clip = blockIdx.y;
+  if (threadIdx.x < 64) {
+    float mx = -INFINITY;
+    for (int g = threadIdx.x; g < kMelGroups; g += 64)
+      mx = fmaxf(mx, group_max[(int64_t)clip * kMelGroups + g]);
+    mx = wave_max(mx);
+    if (threadIdx.x == 0) s_floor = mx - 8.0f;
+  }
+  __syncthreads();
+  const float floor_v = s_floor;
+  const int64_t n_in = (int64_t)kFrames * n_mels, shift = (int64_t)pad_rows * n_mels;
+  const int64_t n_out = n_in + 2 * shift;
+  const float* src = mel_raw + (int64_t)clip * n_in;
+  T* dst = out + (int64_t)clip * n_out;
+  for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < n_out / V;
+       q += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t j = V * q - shift;   // input element of output element V q
+    if (V == 4) {
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (j >= 0 && j < n_in) {
+        v = *(const float4*)(src + j);
+        v.x = (fmaxf(v.x, floor_v) + 4.0f) * 0.25f;
+        v.y = (fmaxf(v.y, floor_v) + 4.0f) * 0.25f;
+        v.z = (fmaxf(v.z, floor_v) + 4.0f) * 0.25f;
+        v.w = (fmaxf(v.w, floor_v) + 4.0f) * 0.25f;
+      }
+      St<T>::st4(dst, V * q, v);
+    } else {
+      const float v = j >= 0 && j < n_in ? (fmaxf(src[j], floor_v) + 4.0f) * 0.25f : 0.0f;
+      St<T>::st(dst, q, v);
     }
-    St<T>::st(out, (int64_t)clip * n + i, v);
   }
 }
 template <typename T>
-void mel_normalize(const float* mel_raw, const uint32_t* clip_max, int n_clips, int n_mels,
+void mel_normalize(const float* mel_raw, const float* group_max, int n_clips, int n_mels,
                    T* out, int pad_rows, hipStream_t s) {
   if (n_clips <= 0) return;
-  int64_t n = (int64_t)(kFrames + 2 * pad_rows) * n_mels;
-  dim3 grid((unsigned)((n + 255) / 256 > 4096 ? 4096 : (n + 255) / 256), n_clips);
-  k_mel_norm<T><<<grid, 256, 0, s>>>(mel_raw, clip_max, n_mels, out, pad_rows);
+  const bool vec = (uintptr_t)mel_raw % 16 == 0 && (uintptr_t)out % (4 * sizeof(T)) == 0;
+  const int V = vec ? 4 : 1;
+  const int64_t nv = (int64_t)(kFrames + 2 * pad_rows) * n_mels / V;
+  // about 16 vectors per thread, so the maximum's reduction is a small part of a block
+  dim3 grid((unsigned)((nv + 256 * 16 - 1) / (256 * 16)), n_clips);
+  if (vec)
+    k_mel_norm<T, 4><<<grid, 256, 0, s>>>(mel_raw, group_max, n_mels, out, pad_rows);
+  else
+    k_mel_norm<T, 1><<<grid, 256, 0, s>>>(mel_raw, group_max, n_mels, out, pad_rows);
 }
-template void mel_normalize<float>(const float*, const uint32_t*, int, int, float*, int,
+template void mel_normalize<float>(const float*, const float*, int, int, float*, int,
                                    hipStream_t);
-template void mel_normalize<bf16_t>(const float*, const uint32_t*, int, int, bf16_t*, int,
+template void mel_normalize<bf16_t>(const float*, const float*, int, int, bf16_t*, int,
                                     hipStream_t);
 
 }  // namespace asr

@@ -82,7 +82,7 @@ struct Layout {
   size_t window = 0, cos_t = 0, sin_t = 0, fb = 0, fb_range = 0, sinus = 0;
   size_t self_kv = 0, cross_kv = 0;
   int64_t self_stride = 0, cross_stride = 0;   // elements per slot
-  size_t pcm_stage = 0, pcm_ptrs = 0, pcm_n = 0, mel_raw = 0, clip_max = 0, mel_norm = 0,
+  size_t pcm_stage = 0, pcm_ptrs = 0, pcm_n = 0, mel_raw = 0, mel_gmax = 0, mel_norm = 0,
          h1 = 0, x = 0, xn = 0, qkv = 0, vt = 0, att = 0, hid = 0, p_slots = 0;
   size_t vt_bytes = 0;
   size_t d_slots = 0, d_tokens = 0, d_pos = 0, d_h = 0, d_xn = 0, d_qkv = 0, d_att = 0,
@@ -277,7 +277,7 @@ void plan(asr_ctx* c) {
   L.window = b.take(kNFFT * f4);
   L.cos_t = b.take(kNFFT * f4);
   L.sin_t = b.take(kNFFT * f4);
-  L.fb = b.take(M * kBins * f4);
+  L.fb = b.take(2 * kBins * f4);   // packed: at most two filters per bin
   L.fb_range = b.take(M * 3 * 4);
   L.sinus = b.take((int64_t)kCtx * d * f4);
   // per-slot caches [slot][n_dec][2][H][ctx][64]
@@ -292,7 +292,7 @@ void plan(asr_ctx* c) {
   L.pcm_ptrs = b.take(P * 8);
   L.pcm_n = b.take(P * 8);
   L.mel_raw = b.take(P * kFrames * M * f4);
-  L.clip_max = b.take(P * 4);
+  L.mel_gmax = b.take(P * kMelGroups * 4);
   L.mel_norm = b.take(P * (kFrames + 2) * M * std::max<size_t>(es, f4));
   L.h1 = b.take(P * (kFrames + 1) * d * es);
   L.x = b.take(R * d * f4);
@@ -411,6 +411,9 @@ HostMelTables host_mel_tables(int M) {
 asr_status upload_tables(asr_ctx* c) {
   const int M = c->cfg.n_mels, d = c->cfg.d_model;
   const HostMelTables mt = host_mel_tables(M);
+  // the kernel stages the packed weights in LDS sized for two per bin (every
+  // bin lies in at most two triangular filters)
+  if (mt.fb.size() > 2 * kBins) return fail(ASR_EINVAL, "packed filterbank larger than two weights per bin");
   const std::vector<float>&win = mt.win, &ct = mt.ct, &st = mt.st, &fb = mt.fb;
   const std::vector<int32_t>& rng = mt.rng;
   std::vector<float> sin_tab((size_t)kCtx * d);
@@ -550,7 +553,7 @@ asr_status run_mel(asr_ctx* c, int n) {
   bytes = (double)n * kSamples30s * 4 + (double)n * kFrames * M * 4;
   timed(c, ASR_K_MEL, (double)n * kFrames * kBins * kNFFT * 4.0, bytes, [&] {
     log_mel(c->at<const float* const>(c->L.pcm_ptrs), c->at<int64_t>(c->L.pcm_n), n, M, t,
-            c->at<float>(c->L.mel_raw), c->at<uint32_t>(c->L.clip_max), c->stream);
+            c->at<float>(c->L.mel_raw), c->at<float>(c->L.mel_gmax), c->stream);
   });
   CHECK_LAUNCH();
   return ASR_OK;
@@ -621,7 +624,7 @@ asr_status encode_clips(asr_ctx* c, int n, bool xkv = false) {
   asr_status st = run_mel(c, n);
   if (st != ASR_OK) return st;
   timed(c, ASR_K_MEL, 0.0, (double)n * kFrames * Mm * (4 + c->es), [&] {
-    mel_normalize<T>(c->at<float>(L.mel_raw), c->at<uint32_t>(L.clip_max), n, Mm,
+    mel_normalize<T>(c->at<float>(L.mel_raw), c->at<float>(L.mel_gmax), n, Mm,
                      c->at<T>(L.mel_norm), 1, c->stream);
   });
   float* x_all = c->at<float>(L.x);
@@ -1712,7 +1715,7 @@ asr_status asr_debug_logmel(asr_ctx* c, const float* const* pcm, const int64_t* 
   st = run_mel(c, n);
   if (st != ASR_OK) return st;
   float* tmp = c->at<float>(c->L.wstage);
-  mel_normalize<float>(c->at<float>(c->L.mel_raw), c->at<uint32_t>(c->L.clip_max), n,
+  mel_normalize<float>(c->at<float>(c->L.mel_raw), c->at<float>(c->L.mel_gmax), n,
                        c->cfg.n_mels, tmp, 0, c->stream);
   CHECK_LAUNCH();
   HIPCHK(hipMemcpyAsync(out, tmp, (size_t)n * kFrames * c->cfg.n_mels * 4, hipMemcpyDeviceToHost,
@@ -1886,11 +1889,12 @@ namespace {
 constexpr int kNaDevices = 64;
 // word offsets into the scratch array
 constexpr size_t kNaWin = 0, kNaCos = kNaWin + kNFFT, kNaSin = kNaCos + kNFFT;
-constexpr size_t kNaFb80 = kNaSin + kNFFT, kNaFb128 = kNaFb80 + (size_t)80 * kBins;
-constexpr size_t kNaRng80 = kNaFb128 + (size_t)128 * kBins, kNaRng128 = kNaRng80 + 3 * 80;
-constexpr size_t kNaMax = kNaRng128 + 3 * 128;
-constexpr size_t kNaWords = kNaMax + kMelArgClips;
-constexpr size_t kNaBytes = 192 * 1024;   // the stated maximum: 192 KiB per GPU
+// (packed filter weights: every bin lies in at most two filters)
+constexpr size_t kNaFb80 = kNaSin + kNFFT, kNaFb128 = kNaFb80 + 2 * kBins;
+constexpr size_t kNaRng80 = kNaFb128 + 2 * kBins, kNaRng128 = kNaRng80 + 3 * 80;
+constexpr size_t kNaMax = kNaRng128 + 3 * 128;   // group maxima [clips][kMelGroups]
+constexpr size_t kNaWords = kNaMax + (size_t)kMelArgClips * kMelGroups;
+constexpr size_t kNaBytes = 64 * 1024;   // the stated maximum: 64 KiB per GPU
 static_assert(kNaWords * 4 <= kNaBytes, "scratch layout");
 
 }  // namespace
@@ -1912,6 +1916,8 @@ asr_status na_setup(int dev, uint32_t** out) {
     if (!p) return fail(ASR_EDEVICE, "hipGetSymbolAddress returned NULL");
     uint32_t* base = (uint32_t*)p;
     const HostMelTables t80 = host_mel_tables(80), t128 = host_mel_tables(128);
+    if (t80.fb.size() > 2 * kBins || t128.fb.size() > 2 * kBins)
+      return fail(ASR_EINVAL, "packed filterbank larger than two weights per bin");
     HIPCHK(hipMemcpy(base + kNaWin, t80.win.data(), kNFFT * 4, hipMemcpyHostToDevice));
     HIPCHK(hipMemcpy(base + kNaCos, t80.ct.data(), kNFFT * 4, hipMemcpyHostToDevice));
     HIPCHK(hipMemcpy(base + kNaSin, t80.st.data(), kNFFT * 4, hipMemcpyHostToDevice));
@@ -1954,8 +1960,9 @@ extern "C" asr_status asr_logmel_noalloc(const float* const* pcm, const int64_t*
               (const int32_t*)(base + (wide ? kNaRng128 : kNaRng80))};
   hipStream_t s = (hipStream_t)stream;
   // raw log-mel straight into out, then the clamp and affine in place
-  log_mel_args(clips, n, n_mels, t, out, base + kNaMax, s);
-  mel_normalize<float>(out, base + kNaMax, n, n_mels, out, 0, s);
+  float* gmax = (float*)(base + kNaMax);
+  log_mel_args(clips, n, n_mels, t, out, gmax, s);
+  mel_normalize<float>(out, gmax, n, n_mels, out, 0, s);
   CHECK_LAUNCH();
   return ASR_OK;
 }

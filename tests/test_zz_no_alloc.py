@@ -1,8 +1,10 @@
 """The allocation-free log-mel entry point (asr_logmel_noalloc) against the
 existing one (asr_debug_logmel), through the C ABI: the same kernels on the
-same clips, so the features must agree bit for bit; two calls in a row, the
+same clips, so the features must agree bit for bit; calls in a row, the
 second with fewer and shorter clips (the shared scratch keeps the first
-call's per-clip maxima, which the second must clear)."""
+call's per-group maxima, which the second must overwrite before it reads
+them), the third into an output one float past a 16-byte boundary (the
+normalisation's unvectorised path)."""
 import numpy as np
 import pytest
 import torch
@@ -29,20 +31,22 @@ def test_noalloc_logmel_matches_bound_entry_point(n_mels):
     first = [480000, 64000, 1, 16000, 123457, 480000]
     second = [32000, 7]
     ctx = _ctx(n_mels, len(first))
-    for lengths in (first, second):
+    for lengths, offset in ((first, 0), (second, 0), (second, 1)):
         clips = [synth.pcm_clip(seed, i, n) for i, n in enumerate(lengths)]
         if len(lengths) > 3:
             clips[3] = np.zeros(lengths[3], np.float32)        # silence: the constant floor
         dev = [torch.from_numpy(c).cuda() for c in clips]
-        out = torch.full((len(clips), 3000, n_mels), float("nan"), dtype=torch.float32,
-                         device="cuda")
+        size = len(clips) * 3000 * n_mels
+        buf = torch.full((size + offset,), float("nan"), dtype=torch.float32, device="cuda")
+        out = buf[offset:].view(len(clips), 3000, n_mels)
         asr.logmel_noalloc(dev, n_mels, out)
         torch.cuda.synchronize()
         got = out.cpu().numpy()
         ref = ctx.debug_logmel(clips)
         assert not np.isnan(got).any()
         assert np.array_equal(got, ref), f"max diff {np.abs(got - ref).max():.3e}"
-        print(f"n_mels {n_mels}, {len(clips)} clips: bit-identical to asr_debug_logmel")
+        print(f"n_mels {n_mels}, {len(clips)} clips, output offset {offset}: "
+              "bit-identical to asr_debug_logmel")
 
 
 def test_noalloc_logmel_rejects_bad_sizes():
