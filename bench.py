@@ -74,10 +74,6 @@ def parse():
     ap.add_argument("--no-serving", action="store_true",
                     help="skip the continuous-batching run and the serving simulation")
     ap.add_argument("--cpu-budget-s", type=float, default=25.0)
-    ap.add_argument("--zero-inputs", action="store_true",
-                    help="zero-filled weights, caches and audio instead of the seeded "
-                         "generator: same launches and memory traffic, for hardware-counter "
-                         "runs only (values are meaningless)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (3 times): the reference "
                          "reading for the FETCH_SIZE / WRITE_SIZE counters")
@@ -119,11 +115,7 @@ def main():
     log(f"workspace {ctx.workspace_size() / 2**30:.1f} GiB")
     ctx.bind()
     t0 = time.time()
-    if args.zero_inputs:
-        params = {n: torch.zeros(shp, dtype=torch.float32, device=dev)
-                  for n, shp, _ in synth.param_specs(shape)}
-    else:
-        params = synth.model_params(shape, enc_wl.seed, device=dev)
+    params = synth.model_params(shape, enc_wl.seed, device=dev)
     ctx.load_weights(list(params.values()), on_device=True)
     torch.cuda.synchronize()
     log(f"weights generated + loaded in {time.time() - t0:.1f} s")
@@ -148,30 +140,21 @@ def main():
     t0 = time.time()
     for s0 in range(0, D, P):
         idx = list(range(s0, min(D, s0 + P)))
-        if args.zero_inputs:
-            E = torch.zeros((len(idx), synth.N_AUDIO_CTX, shape.d_model), device=dev)
-        else:
-            E = torch.stack([synth.encoder_output(dec_wl.seed, b, shape.d_model, device=dev)
-                             for b in idx])
+        E = torch.stack([synth.encoder_output(dec_wl.seed, b, shape.d_model, device=dev)
+                         for b in idx])
         ctx.debug_set_encoder_out(idx, [-1] * len(idx), [steps_left[b] for b in idx], E,
                                   on_device=True)
         del E
     for b in range(D):
-        if args.zero_inputs:
-            kv = torch.zeros((shape.n_dec, 2, shape.n_head, synth.N_TEXT_CTX, 64), device=dev)
-        else:
-            kv = synth.self_kv_prefix(dec_wl.seed, b, shape.n_dec, shape.n_head, device=dev)
+        kv = synth.self_kv_prefix(dec_wl.seed, b, shape.n_dec, shape.n_head, device=dev)
         ctx.debug_set_self_kv(b, kv, int(kv_len[b]), on_device=True)
         del kv
     torch.cuda.synchronize()
     log(f"{D} decode slots filled in {time.time() - t0:.1f} s")
 
     # -------------------------------------------------- prefill audio in HBM
-    if args.zero_inputs:
-        pcm_host = np.zeros((P, synth.N_SAMPLES_30S), np.float32)
-    else:
-        pcm_host = np.stack([synth.pcm_clip(enc_wl.seed, i, synth.N_SAMPLES_30S)
-                             for i in range(P)])
+    pcm_host = np.stack([synth.pcm_clip(enc_wl.seed, i, synth.N_SAMPLES_30S)
+                         for i in range(P)])
     pcm = torch.from_numpy(pcm_host).to(dev)
     toks = synth.token_ids(dec_wl.seed, (args.warmup + args.steps + max(1, args.breakdown_steps), D),
                            shape.vocab)
@@ -295,12 +278,10 @@ def main():
                             "achieved": round(dattn_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                             "frac": round(dattn_gbs / PEAK_HBM_GBS, 4), "traffic": None},
     }
-    if args.zero_inputs:
-        result["data"] = "zero-filled (hardware-counter run; values meaningless)"
-    if not args.no_serving and not args.zero_inputs:
+    if not args.no_serving:
         result["serving"] = serving_section(ctx, D, P, enc_ms, dec_ms, toks,
                                             args.warmup + args.steps + nb)
-    if not args.no_cpu_baseline and not args.zero_inputs:
+    if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(shape, enc_wl, dec_wl, pcm_host[0], P, D,
                                               ms_step, args.cpu_budget_s)
     print(json.dumps(result), flush=True)

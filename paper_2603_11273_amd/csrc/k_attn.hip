@@ -4,8 +4,8 @@
 //    30-s segment (no mask), MFMA-based.  Each wave owns 32 queries; K and
 //    V^T tiles of 64 keys are staged in LDS and shared by the block's
 //    waves.  The kernel computes S^T = K Q^T so that, in the MFMA output
-//    layout, each lane holds one query's scores for 16 keys: the row max and
-//    sum need a single cross-lane exchange, the probabilities feed the
+//    layout, each lane holds one query's scores for 32 keys: the row max
+//    needs a single cross-lane exchange, the probabilities feed the
 //    O^T = V^T P^T product directly as its B operand, and the per-query
 //    rescale is a per-lane multiply.  Softmax runs in fp32 with exp2.
 //  * flash_attn_f32: the same result in plain fp32 (one thread per query).
@@ -26,37 +26,59 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) {
 // ---------------------------------------------------------------------------
 // Encoder flash attention (bf16)
 //
-// Block = NW waves x 32 queries of one (clip, head); tiles of 64 keys.  K
+// Block = 8 waves x 32 queries of one (clip, head); tiles of 64 keys.  K
 // comes from the fused QKV buffer, V from the per-head transposed copy the
-// QKV GEMM writes (V^T[dim][position], zero past 1500), so both tiles are
-// plain 16-byte row copies into LDS (XOR-swizzled rows, conflict-free).
-// S^T = K Q^T is computed per 32-key x 32-query block: in the MFMA output
-// layout a lane owns one query and 16 keys, so the row max needs one
-// cross-lane exchange (lane ^ 32), the probabilities (bf16) are directly the
-// B operand of O^T += V^T P^T, and the online-softmax rescale is per lane.
-// Q arrives scaled by 1/sqrt(64) log2(e), so scores are already in the exp2
-// domain; only the last key tile needs the position mask.
+// QKV GEMM writes (V^T[dim][position], zero past 1500).  S^T = K Q^T is
+// computed per 32-key x 32-query block, so in the MFMA output layout a lane
+// owns one query: the row max needs one cross-lane exchange (lane ^ 32) and
+// the online-softmax rescale is per lane.
+//  * The K rows of each 32-key block enter the MFMA in the order that swaps
+//    bits 2 and 3 of the row index.  A lane then holds its query's scores
+//    for 8 consecutive keys per 16-key group, which, packed to bf16, are
+//    directly the B operand of O^T += V^T P^T; the matching A operand is one
+//    16-byte chunk of a V^T row.  Both tiles are plain [row][64] bf16 tiles
+//    with 16-byte chunks XOR-swizzled by (row / 2) % 8 (conflict-free
+//    fragment reads), double-buffered in LDS and filled by direct
+//    global-to-LDS loads (one 1 KB instruction per wave per operand): tile
+//    kt+1 is in flight while tile kt is consumed, one barrier per tile.
+//  * The probability sum uses v_dot2 on the packed bf16 probabilities (the
+//    same rounded values the P V product uses), two per instruction.
+//  * Q arrives scaled by 1/sqrt(64) log2(e) (the QKV epilogue folds the
+//    factor in before its one bf16 rounding), so scores are in the exp2
+//    domain; softmax in fp32 with exp2 and a lazy reference (below).
+// The kernel keeps to 128 VGPRs (four waves per SIMD, two blocks per CU):
+// the exp2 work on the VALU and the MFMAs of other waves then overlap.
 // ---------------------------------------------------------------------------
-constexpr int FA_KT = 64;          // keys per tile
+constexpr int FP_NW = 8, FP_KT = 64;
 
-__device__ __forceinline__ int fa_swz(int row) { return (row >> 1) & 7; }
+__device__ __forceinline__ void fp_dma16(uint32_t lds_addr, uint32_t voff, const void* sbase) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :: "s"(lds_addr), "v"(voff), "s"(sbase) : "memory", "m0");
+}
+template <int N>
+__device__ __forceinline__ void fp_wait_vmcnt() {
+  static_assert(N >= 0 && N < 16, "vmcnt");
+  __builtin_amdgcn_s_waitcnt(N | (0x7 << 4) | (0xF << 8));
+}
+// row index of the K tile that feeds MFMA row i (bits 2 and 3 swapped)
+__device__ __forceinline__ int fp_perm(int i) {
+  return (i & ~12) | ((i & 4) << 1) | ((i & 8) >> 1);
+}
 
-template <int NW>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) void k_flash_bf16(const bf16_t* __restrict__ qkv,
-                                                       const bf16_t* __restrict__ vt,
-                                                       bf16_t* __restrict__ out, int n_head) {
-  constexpr int NTH = NW * 64;
-  constexpr int CPT = 512 / NTH;                   // 16-byte chunks per thread per operand tile
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][FA_KT * 64];   // [key][dim]
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[2][64 * FA_KT];   // [dim][key]
+__global__ __launch_bounds__(FP_NW * 64) __attribute__((amdgpu_waves_per_eu(4)))
+void k_flash_bf16(const bf16_t* __restrict__ qkv, const bf16_t* __restrict__ vt,
+                       bf16_t* __restrict__ out, int n_head) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  constexpr int S = 2;                             // LDS stages
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[S][FP_KT * 64];   // [key][dim]
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[S][64 * FP_KT];   // [dim][key]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = blockIdx.y, b = blockIdx.z;
   const int d = n_head * 64, ld3 = 3 * d;
   const bf16_t* base = qkv + (int64_t)b * kCtx * ld3;
-  const bf16_t* vbase = vt + ((int64_t)b * n_head + h) * 64 * kVtLd;
   const int half = lane >> 5, l32 = lane & 31;
-  const int q = blockIdx.x * (NW * 32) + wave * 32 + l32;   // this lane's query
-  const uint4 z = {0u, 0u, 0u, 0u};
+  const int q = blockIdx.x * (FP_NW * 32) + wave * 32 + l32;   // this lane's query
+  constexpr int NT = (kCtx + FP_KT - 1) / FP_KT;
 
   // Q fragments (B operand of S^T): dims kk*16 + half*8 .. +8 of query q
   bf16x8 qf[4];
@@ -64,89 +86,92 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
     const bf16_t* qp = base + (int64_t)(q < kCtx ? q : 0) * ld3 + h * 64 + half * 8;
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      uint4 v = z;
+      uint4 v = {0u, 0u, 0u, 0u};
       if (q < kCtx) v = *(const uint4*)(qp + kk * 16);
       qf[kk] = as_bf16x8(v);
     }
   }
 
-  // tile loader: chunk c of K (rows = keys) and of V^T (rows = dims); a chunk
-  // is 8 consecutive elements of one 64-element row
-  uint4 rk[CPT], rv[CPT];
-#define FA_GLOAD(k0)                                                                \
-  do {                                                                              \
-    _Pragma("unroll") for (int u = 0; u < CPT; ++u) {                               \
-      const int c = tid + u * NTH, row = c >> 3, ch = c & 7;                        \
-      const int key = (k0) + row;                                                   \
-      rk[u] = z;                                                                    \
-      if (key < kCtx) rk[u] = *(const uint4*)(base + (int64_t)key * ld3 + d + h * 64 + ch * 8); \
-      rv[u] = *(const uint4*)(vbase + (int64_t)row * kVtLd + (k0) + ch * 8);        \
-    }                                                                               \
-  } while (0)
-  // V^T rows keep their two 8-byte halves swapped when bit 4 XOR bit 5 of
-  // the row is set: the 8-byte fragment reads of 32 consecutive rows then hit
-  // distinct banks, and a lane's reads of rows r and r + 32 are never a
-  // whole number of 512-byte steps apart (the compiler would pair such reads
-  // into one two-address instruction whose halves share banks)
-#define FA_SSTORE(buf)                                                              \
-  do {                                                                              \
-    _Pragma("unroll") for (int u = 0; u < CPT; ++u) {                               \
-      const int c = tid + u * NTH, row = c >> 3, ch = c & 7;                        \
-      const int pos = row * 64 + ((ch ^ fa_swz(row)) * 8);                          \
-      *(uint4*)&Ks[buf][pos] = rk[u];                                               \
-      const uint4 v = rv[u];                                                        \
-      *(uint4*)&Vs[buf][pos] = (((row >> 4) ^ (row >> 5)) & 1) ? uint4{v.z, v.w, v.x, v.y} : v; \
-    }                                                                               \
-  } while (0)
+  // Direct loads: wave w fills rows 8w .. 8w+7 of both tiles; lane l lands
+  // 16 bytes at slot l % 8 of row 8w + l / 8 and fetches the chunk that the
+  // swizzle puts there.  K rows past position 1499 re-read row 1499 (their
+  // scores are masked); V^T rows are padded to kVtLd >= 64 NT positions.
+  const int lrow = wave * 8 + (lane >> 3);
+  const int lch = (lane & 7) ^ ((lrow >> 1) & 7);
+  const uint32_t k_lds = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16_t*)&Ks[0][0] + (uint32_t)(wave * 1024));
+  const uint32_t v_lds = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16_t*)&Vs[0][0] + (uint32_t)(wave * 1024));
+  const bf16_t* kbase = base + d + h * 64;                          // K columns of head h
+  const bf16_t* vbase = vt + ((int64_t)b * n_head + h) * 64 * kVtLd;
+  const uint32_t v_off = (uint32_t)((lrow * kVtLd + lch * 8) * 2);
+  auto issue = [&](int t) {
+    const int k0 = t * FP_KT;
+    const int key = min(k0 + lrow, kCtx - 1);
+    const uint32_t so = (uint32_t)((t % S) * FP_KT * 64 * 2);
+    fp_dma16(k_lds + so, (uint32_t)((key * ld3 + lch * 8) * 2), kbase);
+    fp_dma16(v_lds + so, v_off, vbase + k0);
+  };
+
+  // fragment read offsets (elements) within a stage
+  const int sw = (l32 >> 1) & 7;                       // swizzle of rows l32 and 32 + l32
+  int koff[2][4];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    const int row = kb * 32 + fp_perm(l32);
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) koff[kb][kk] = row * 64 + (((kk * 2 + half) ^ ((row >> 1) & 7)) * 8);
+  }
+
+  f32x16 zero16;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) zero16[r] = 0.f;
+  // all eight K fragments in flight before the first MFMA needs one
+  // scores of tile t: four K fragments in flight per 32-key block
+  auto scores = [&](int t, f32x16 (&s)[2]) {
+    const bf16_t* Kc = Ks[t % S];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      bf16x8 kf[4];
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) kf[kk] = *(const bf16x8*)(Kc + koff[kb][kk]);
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk)
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk],
+                                                        kk == 0 ? zero16 : s[kb], 0, 0, 0);
+    }
+  };
 
   f32x16 o0, o1;                                   // O^T dims 0..31, 32..63
 #pragma unroll
   for (int r = 0; r < 16; ++r) o0[r] = o1[r] = 0.f;
-  // Q arrives pre-scaled by 1/sqrt(64) * log2(e) (the QKV product's epilogue
-  // folds the factor in before its one bf16 rounding), so scores are in the
-  // exp2 domain.
   float m = 0.f, l = 0.f;
   bool zref = true;                                // every lane of the wave has m == 0
-  f32x16 zero16;
-#pragma unroll
-  for (int r = 0; r < 16; ++r) zero16[r] = 0.f;
-  const int sw = fa_swz(l32);
-  const int vhalf = (half ^ ((l32 >> 4) & 1)) * 4;
+  const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3F803F80u);
 
-  constexpr int NT = (kCtx + FA_KT - 1) / FA_KT;
-  FA_GLOAD(0);
-  FA_SSTORE(0);
-  __syncthreads();
-  for (int kt = 0; kt < NT; ++kt) {
-    const int cur = kt & 1;
-    const int k0 = kt * FA_KT;
-    if (kt + 1 < NT) FA_GLOAD(k0 + FA_KT);
-    const bf16_t* Kc = Ks[cur];
-    const bf16_t* Vc = Vs[cur];
-
-    f32x16 s[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const bf16x8 kf =
-            *(const bf16x8*)(Kc + (kb * 32 + l32) * 64 + (((kk * 2 + half) ^ sw) * 8));
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], kk == 0 ? zero16 : s[kb], 0,
-                                                        0, 0);
-      }
-    }
+  // softmax of tile t's scores (in s) and its P V product
+  // (the rare branches carry an empty volatile asm so that the compiler
+  // keeps them as branches instead of executing them on every tile)
+  auto consume = [&](int t, f32x16 (&s)[2]) {
+    const int k0 = t * FP_KT;
+    // V fragments: chunk kb*4 + hf*2 + half of V^T rows l32 and 32 + l32
+    const bf16_t* Vc = Vs[t % S];
+    auto vfrag = [&](int kb, int hf, int row) {
+      return *(const bf16x8*)(Vc + row * 64 + (((kb * 4 + hf * 2 + half) ^ sw) * 8));
+    };
     if (!zref) {                                   // wave-uniform: some lane's m moved
+      asm volatile("");
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[kb][r] -= m;
     }
-    if (k0 + FA_KT > kCtx) {                       // last tile: keys past 1500 do not exist
+    if (k0 + FP_KT > kCtx) {                       // last tile: keys past 1500 do not exist
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int key = k0 + kb * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
+          const int key = k0 + kb * 32 + (r >> 3) * 16 + half * 8 + (r & 7);
           if (key >= kCtx) s[kb][r] = -INFINITY;
         }
     }
@@ -163,8 +188,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
     // (both reach 2^127); the final 1/l cancels the offset.  A first tile
     // whose maximum lies outside [-64, 64] sets m to it; a later score more
     // than 2^6 above m moves m up and rescales O and l.
-    if (kt == 0) {
+    if (t == 0) {
       if (__any(fabsf(tmax) > 64.0f)) {            // 64 real keys: finite
+        asm volatile("");
         m = tmax;
         zref = false;
 #pragma unroll
@@ -173,6 +199,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
           for (int r = 0; r < 16; ++r) s[kb][r] -= tmax;
       }
     } else if (__any(tmax > 64.0f)) {
+      asm volatile("");
       const float shift = fmaxf(tmax, 0.f);
       const float alpha = __builtin_amdgcn_exp2f(-shift);
       m += shift;
@@ -188,47 +215,34 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[kb][r] -= shift;
     }
-    float psum = 0.f;
-    bf16x8 pb[2][2];                               // [kb][hf]
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
-        float p[8];
+        // keys kb*32 + hf*16 + half*8 .. +8: registers hf*8 .. hf*8+7
+        uint32_t u[4];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          // exp2 of a value <= 64; results below 2^-126 flush to 0, far below
-          // the bf16 resolution of a probability next to the row's maximum
-          p[i] = __builtin_amdgcn_exp2f(s[kb][hf * 8 + i]);
-          psum += p[i];
+        for (int i = 0; i < 4; ++i) {
+          u[i] = pack2_bf16(__builtin_amdgcn_exp2f(s[kb][hf * 8 + 2 * i]),
+                            __builtin_amdgcn_exp2f(s[kb][hf * 8 + 2 * i + 1]));
+          l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u[i]), ones, l, false);
         }
-        uint4 u = {pack2_bf16(p[0], p[1]), pack2_bf16(p[2], p[3]), pack2_bf16(p[4], p[5]),
-                   pack2_bf16(p[6], p[7])};
-        pb[kb][hf] = as_bf16x8(u);
+        const bf16x8 pb = as_bf16x8(uint4{u[0], u[1], u[2], u[3]});
+        o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(kb, hf, l32), pb, o0, 0, 0, 0);
+        o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(kb, hf, 32 + l32), pb, o1, 0, 0, 0);
       }
-    l += psum;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-        // keys kb*32 + hf*16 + half*4 + {0..3} and + 8: chunks c, c+1 of the V^T row
-        const int c = kb * 4 + hf * 2;
-        const bf16_t* v0 = Vc + l32 * 64;
-        const bf16_t* v1 = Vc + (32 + l32) * 64;
-        const uint2 a0 = *(const uint2*)(v0 + ((c ^ sw) * 8) + vhalf);
-        const uint2 a1 = *(const uint2*)(v0 + (((c + 1) ^ sw) * 8) + vhalf);
-        const uint2 c0 = *(const uint2*)(v1 + ((c ^ sw) * 8) + (vhalf ^ 4));
-        const uint2 c1 = *(const uint2*)(v1 + (((c + 1) ^ sw) * 8) + (vhalf ^ 4));
-        o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(uint4{a0.x, a0.y, a1.x, a1.y}),
-                                                     pb[kb][hf], o0, 0, 0, 0);
-        o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(uint4{c0.x, c0.y, c1.x, c1.y}),
-                                                     pb[kb][hf], o1, 0, 0, 0);
-      }
-    if (kt + 1 < NT) FA_SSTORE(cur ^ 1);
-    __syncthreads();
+  };
+
+  // tile t+1 loads while tile t is consumed
+  f32x16 sc[2];
+  issue(0);
+  for (int t = 0; t < NT; ++t) {
+    fp_wait_vmcnt<0>();                            // tile t landed
+    __syncthreads();                               // ... for every wave; tile t-1's stage free
+    if (t + 1 < NT) issue(t + 1);
+    scores(t, sc);
+    consume(t, sc);
   }
-#undef FA_GLOAD
-#undef FA_SSTORE
   l += __shfl_xor(l, 32, 64);
   if (q >= kCtx) return;
   const float inv = 1.0f / l;
@@ -248,9 +262,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
 void flash_attn_bf16(const bf16_t* qkv, const bf16_t* vt, bf16_t* out, int B, int n_head,
                      hipStream_t s) {
   if (B <= 0) return;
-  constexpr int NW = 8;
-  dim3 grid((kCtx + NW * 32 - 1) / (NW * 32), n_head, B);
-  k_flash_bf16<NW><<<grid, NW * 64, 0, s>>>(qkv, vt, out, n_head);
+  static_assert(kVtLd >= FP_KT * ((kCtx + FP_KT - 1) / FP_KT), "V^T rows cover every tile");
+  dim3 grid((kCtx + FP_NW * 32 - 1) / (FP_NW * 32), n_head, B);
+  k_flash_bf16<<<grid, FP_NW * 64, 0, s>>>(qkv, vt, out, n_head);
 }
 
 // Lays given q / k / v ([B*1500][d] float32) out as the encoder attention
