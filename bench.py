@@ -217,7 +217,8 @@ def main():
     enc_ms = tm["prefill"]["ms"] / args.steps
     encode_ms = tm["encode"]["ms"] / args.steps
     dec_ms = tm["decode"]["ms"] / args.steps
-    g = tb["gemm"]
+    # every MFMA GEMM launch: encoder and stem products plus the cross K/V product
+    g = {k: tb["gemm"][k] + tb["xkv"][k] for k in ("ms", "flops", "launches")}
     gemm_tflops = g["flops"] / (g["ms"] * 1e-3) / 1e12 if g["ms"] else 0.0
     da = tb["dattn"]
     dattn_gbs = da["bytes"] / (da["ms"] * 1e-3) / 1e9 if da["ms"] else 0.0

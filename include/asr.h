@@ -190,7 +190,7 @@ asr_status asr_slot_info(const asr_ctx* ctx, int32_t slot, int32_t* occupied, in
 /* ---- per-kernel timing (HIP events around every launch on the bound stream) */
 typedef enum {
   ASR_K_MEL = 0,        /* log-mel front-end (+ normalise) */
-  ASR_K_GEMM = 1,       /* encoder / stem / cross-K/V MFMA GEMMs */
+  ASR_K_GEMM = 1,       /* encoder and stem MFMA GEMMs */
   ASR_K_ATTN = 2,       /* encoder flash attention */
   ASR_K_LN = 3,         /* LayerNorms */
   ASR_K_DGEMM = 4,      /* decode GEMMs (+ split-K reduce) */
@@ -201,7 +201,9 @@ typedef enum {
   ASR_K_DECODE = 9,     /* whole decode phase of asr_step (embed .. argmax) */
   ASR_K_ENCODE = 10,    /* encoder part of a prefill (mel .. ln_post, without cross K/V):
                            from its start to the last clip group's ln_post */
-  ASR_K_COUNT = 11
+  ASR_K_XKV = 11,       /* the cross K/V product of a prefill (all decoder layers, one
+                           MFMA GEMM after the encoder's clip groups have joined) */
+  ASR_K_COUNT = 12
 } asr_kernel_class;
 
 /* ---------------------------------------------------------------------------

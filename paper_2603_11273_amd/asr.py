@@ -19,9 +19,9 @@ STATUS_NAMES = ["OK", "EINVAL", "ENOMEM", "EFULL", "ENOTFOUND", "ESTATE", "ENODE
 FCFS, SJF, HRRN = 0, 1, 2
 F32, BF16 = 0, 1
 (K_MEL, K_GEMM, K_ATTN, K_LN, K_DGEMM, K_DATTN, K_VOCAB, K_OTHER, K_PREFILL, K_DECODE,
- K_ENCODE) = range(11)
+ K_ENCODE, K_XKV) = range(12)
 KERNEL_CLASSES = ["mel", "gemm", "attn", "ln", "dgemm", "dattn", "vocab", "other", "prefill",
-                  "decode", "encode"]
+                  "decode", "encode", "xkv"]
 TIME_ALL = (1 << len(KERNEL_CLASSES)) - 1
 
 EXPORTED = [

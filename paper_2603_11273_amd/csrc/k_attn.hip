@@ -557,47 +557,36 @@ __global__ __launch_bounds__(256) void k_decode_combine(const float* __restrict_
   St<T>::st(out, (int64_t)row * n_head * 64 + h * 64 + lane, num / den);
 }
 
-// bf16 decode attention with every K and V row of the block's keys in
-// flight at once: each thread issues the 16-byte loads of its share of all
-// keys (8 lanes per key, 32 keys per pass, NP passes) for K and V before any
-// arithmetic, so the value stream's latency hides behind the scores and the
-// softmax; scores stay in registers (one cross-lane reduction per key), and
-// three block barriers remain.  The query (and, SELF, this step's key and
-// value) is the bias plus the qp_splits float32 partial sums of its product
-// (qp[s][row][...]).  SELF: one block per (row, head) over all position + 1
-// keys, writing the output directly; the new key and value, rounded to bf16,
-// go into the cache at the last position and into the scores from LDS.
-// Cross: one block per (row, head, 384-key chunk), leaving a (max, sum,
-// weighted values) record for the combine kernel.
-template <bool SELF, int NP>
-__global__ __launch_bounds__(256) void k_dattn_bf16(const float* __restrict__ qp, int qp_splits,
-                                                    const float* __restrict__ qp_bias, int D,
-                                                    bf16_t* cache, int64_t slot_stride,
-                                                    int64_t layer_off, const int32_t* slots,
-                                                    const int32_t* pos, int n_head,
-                                                    float* __restrict__ part,
-                                                    bf16_t* __restrict__ out) {
-  constexpr int CTX = SELF ? kTextCtx : kCtx;
+// bf16 decode cross attention with every K and V row of the block's keys
+// in flight at once: each thread issues the 16-byte loads of its share of
+// all keys (8 lanes per key, 32 keys per pass, NP passes) for K and V before
+// any arithmetic, so the value stream's latency hides behind the scores and
+// the softmax; scores stay in registers (one cross-lane reduction per key),
+// and three block barriers remain.  The query is the bias plus the qp_splits
+// float32 partial sums of its product (qp[s][row][d]).  One block per (row,
+// head, 384-key chunk), leaving a (max, sum, weighted values) record for
+// the combine kernel.
+template <int NP>
+__global__ __launch_bounds__(256) void k_dattn_cross_bf16(const float* __restrict__ qp, int qp_splits,
+                                                          const float* __restrict__ qp_bias, int D,
+                                                          const bf16_t* cache, int64_t slot_stride,
+                                                          int64_t layer_off, const int32_t* slots,
+                                                          int n_head, float* __restrict__ part) {
   constexpr int CK = NP * 32;                       // keys per block
   __shared__ float qs[64];
-  __shared__ __attribute__((aligned(16))) bf16_t kvnew[2][64];
   __shared__ float red[2][4];
   __shared__ float ored[4][64];
   const int h = blockIdx.x, row = blockIdx.y, chunk = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int d = n_head * 64;
-  const int n = SELF ? pos[row] + 1 : kCtx;
   const int k0 = chunk * CK;
-  if (k0 >= n) return;
-  const int kn = min(CK, n - k0);
+  const int kn = min(CK, kCtx - k0);
   const int slot = slots[row];
-  bf16_t* kb = cache + (int64_t)slot * slot_stride + layer_off + (int64_t)h * CTX * 64;
-  bf16_t* vb = kb + (int64_t)n_head * CTX * 64;
+  const bf16_t* kb = cache + (int64_t)slot * slot_stride + layer_off + (int64_t)h * kCtx * 64;
+  const bf16_t* vb = kb + (int64_t)n_head * kCtx * 64;
   const int sub = lane >> 3, dc = (lane & 7) * 8;
-  const int ld = SELF ? 3 * d : d;                  // row stride of the partial sums
 
-  // all loads of the block's cached keys first (SELF: the last key is new)
-  const int kcache = SELF ? kn - 1 : kn;
+  // all loads of the block's keys first
   uint4 kr[NP], vr[NP];
   const uint4 zero = {0u, 0u, 0u, 0u};
 #pragma unroll
@@ -605,34 +594,18 @@ __global__ __launch_bounds__(256) void k_dattn_bf16(const float* __restrict__ qp
     const int kk = p * 32 + wave * 8 + sub, key = k0 + kk;
     kr[p] = zero;
     vr[p] = zero;
-    if (kk < kcache) {
+    if (kk < kn) {
       kr[p] = *(const uint4*)(kb + (int64_t)key * 64 + dc);
       vr[p] = *(const uint4*)(vb + (int64_t)key * 64 + dc);
     }
   }
-  // query (and, SELF, the new key and value): bias + the product's partials
-  if (tid < (SELF ? 192 : 64)) {
-    const int part_i = tid >> 6, j = tid & 63;       // 0: q, 1: k, 2: v
-    const int c = part_i * d + h * 64 + j;
+  if (tid < 64) {
+    const int c = h * 64 + tid;
     float v = qp_bias[c];
-    for (int sp = 0; sp < qp_splits; ++sp) v += qp[((int64_t)sp * D + row) * ld + c];
-    if (part_i == 0) {
-      qs[j] = v * 0.125f;
-    } else {
-      const bf16_t b = f2bf(v);
-      kvnew[part_i - 1][j] = b;
-      (part_i == 1 ? kb : vb)[(int64_t)(n - 1) * 64 + j] = b;
-    }
+    for (int sp = 0; sp < qp_splits; ++sp) v += qp[((int64_t)sp * D + row) * d + c];
+    qs[tid] = v * 0.125f;
   }
   __syncthreads();
-  if (SELF) {
-#pragma unroll
-    for (int p = 0; p < NP; ++p)
-      if (p * 32 + wave * 8 + sub == kn - 1) {
-        kr[p] = *(const uint4*)&kvnew[0][dc];
-        vr[p] = *(const uint4*)&kvnew[1][dc];
-      }
-  }
   float qv[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) qv[i] = qs[dc + i];
@@ -689,18 +662,159 @@ __global__ __launch_bounds__(256) void k_dattn_bf16(const float* __restrict__ qp
   if (lane == 0) red[1][wave] = l;
   __syncthreads();
   if (tid < 64) {
-    const float o = ored[0][tid] + ored[1][tid] + ored[2][tid] + ored[3][tid];
-    const float L = red[1][0] + red[1][1] + red[1][2] + red[1][3];
-    if constexpr (SELF) {
-      out[(int64_t)row * d + h * 64 + tid] = f2bf(o / L);
-    } else {
-      float* rec = part + (((int64_t)row * n_head + h) * DA_NCH + chunk) * DA_REC;
-      rec[2 + tid] = o;
-      if (tid == 0) {
-        rec[0] = M;
-        rec[1] = L;
-      }
+    float* rec = part + (((int64_t)row * n_head + h) * DA_NCH + chunk) * DA_REC;
+    rec[2 + tid] = ored[0][tid] + ored[1][tid] + ored[2][tid] + ored[3][tid];
+    if (tid == 0) {
+      rec[0] = M;
+      rec[1] = red[1][0] + red[1][1] + red[1][2] + red[1][3];
     }
+  }
+}
+
+// bf16 decode self attention: one block per (row, head) over the row's
+// position + 1 keys, writing the output directly.  The keys go in two halves
+// of DS_NP passes (224 keys) each, so a thread holds only one half's K and V
+// rows (about 90 VGPRs: five blocks per CU, which is what the short rows'
+// latency needs); the second half, present only for rows longer than 224
+// keys, loads its keys as soon as the first half's scores are done and its
+// values once the first half's weighted sum is, and joins through the usual
+// online-softmax rescale (block-wide maxima, so all lanes share one
+// reference).  The query, key and value of the step are bias + the
+// qp_splits float32 partial sums of the QKV product (qp[s][row][3d]); the new
+// key and value, rounded to bf16, go into the cache at the last position and
+// into the scores from LDS.
+constexpr int DS_NP = 7;
+constexpr int DS_HALF = DS_NP * 32;
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k_dattn_self_bf16(const float* __restrict__ qp, int qp_splits,
+                                                         const float* __restrict__ qp_bias, int D,
+                                                         bf16_t* cache, int64_t slot_stride,
+                                                         int64_t layer_off, const int32_t* slots,
+                                                         const int32_t* pos, int n_head,
+                                                         bf16_t* __restrict__ out) {
+  static_assert(2 * DS_HALF >= kTextCtx, "two halves cover the decoder context");
+  __shared__ float qs[64];
+  __shared__ __attribute__((aligned(16))) bf16_t kvnew[2][64];
+  __shared__ float red[3][4];
+  __shared__ float ored[4][64];
+  const int h = blockIdx.x, row = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int d = n_head * 64;
+  const int n = pos[row] + 1;                       // keys, this step's included
+  const int slot = slots[row];
+  bf16_t* kb = cache + (int64_t)slot * slot_stride + layer_off + (int64_t)h * kTextCtx * 64;
+  bf16_t* vb = kb + (int64_t)n_head * kTextCtx * 64;
+  const int sub = lane >> 3, dc = (lane & 7) * 8;
+  const bool two = n > DS_HALF;                     // block-uniform
+  auto key_of = [&](int hf, int p) { return hf * DS_HALF + p * 32 + wave * 8 + sub; };
+
+  // cached keys (all but the last) of a half
+  uint4 kr[DS_NP], vr[DS_NP];
+  const uint4 zero = {0u, 0u, 0u, 0u};
+  auto load_k = [&](int hf) {
+#pragma unroll
+    for (int p = 0; p < DS_NP; ++p) {
+      const int key = key_of(hf, p);
+      kr[p] = zero;
+      if (key < n - 1) kr[p] = *(const uint4*)(kb + (int64_t)key * 64 + dc);
+    }
+  };
+  auto load_v = [&](int hf) {
+#pragma unroll
+    for (int p = 0; p < DS_NP; ++p) {
+      const int key = key_of(hf, p);
+      vr[p] = zero;
+      if (key < n - 1) vr[p] = *(const uint4*)(vb + (int64_t)key * 64 + dc);
+    }
+  };
+  load_k(0);
+  load_v(0);
+  // query, new key and value: bias + the product's partials
+  if (tid < 192) {
+    const int part_i = tid >> 6, j = tid & 63;       // 0: q, 1: k, 2: v
+    const int c = part_i * d + h * 64 + j;
+    float v = qp_bias[c];
+    for (int sp = 0; sp < qp_splits; ++sp) v += qp[((int64_t)sp * D + row) * 3 * d + c];
+    if (part_i == 0) {
+      qs[j] = v * 0.125f;
+    } else {
+      const bf16_t b = f2bf(v);
+      kvnew[part_i - 1][j] = b;
+      (part_i == 1 ? kb : vb)[(int64_t)(n - 1) * 64 + j] = b;
+    }
+  }
+  __syncthreads();
+  float qv[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) qv[i] = qs[dc + i];
+
+  float M = -INFINITY, l = 0.f, acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+  auto half = [&](int hf) {
+#pragma unroll
+    for (int p = 0; p < DS_NP; ++p)
+      if (key_of(hf, p) == n - 1) {
+        kr[p] = *(const uint4*)&kvnew[0][dc];
+        vr[p] = *(const uint4*)&kvnew[1][dc];
+      }
+    float sc[DS_NP];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int p = 0; p < DS_NP; ++p) {
+      float kv[8];
+      load8((const bf16_t*)&kr[p], kv);
+      float a = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) a = fmaf(qv[i], kv[i], a);
+      a += __shfl_xor(a, 1, 64);
+      a += __shfl_xor(a, 2, 64);
+      a += __shfl_xor(a, 4, 64);
+      sc[p] = key_of(hf, p) < n ? a : -INFINITY;
+      mx = fmaxf(mx, sc[p]);
+    }
+    mx = wave_max(mx);
+    if (lane == 0) red[hf][wave] = mx;
+    __syncthreads();
+    if (hf == 0 && two) load_k(1);                   // the first half's keys are done with
+    const float Mn = fmaxf(M, fmaxf(fmaxf(red[hf][0], red[hf][1]), fmaxf(red[hf][2], red[hf][3])));
+    const float f = expf(M - Mn);                    // 0 on the first half (M = -inf)
+    l *= f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] *= f;
+#pragma unroll
+    for (int p = 0; p < DS_NP; ++p) {
+      const float pr = expf(sc[p] - Mn);             // 0 for keys past the row
+      l += pr;
+      float vv[8];
+      load8((const bf16_t*)&vr[p], vv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[i] = fmaf(pr, vv[i], acc[i]);
+    }
+    M = Mn;
+    if (hf == 0 && two) load_v(1);                   // ... and so are its values
+  };
+  half(0);
+  if (two) half(1);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    float a = acc[i];
+    a += __shfl_xor(a, 8, 64);
+    a += __shfl_xor(a, 16, 64);
+    a += __shfl_xor(a, 32, 64);
+    acc[i] = a;
+  }
+  // each key's probability was added by its 8 lanes
+  l = wave_sum(l) * 0.125f;
+  if (lane < 8) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ored[wave][dc + i] = acc[i];
+  }
+  if (lane == 0) red[2][wave] = l;
+  __syncthreads();
+  if (tid < 64) {
+    const float o = ored[0][tid] + ored[1][tid] + ored[2][tid] + ored[3][tid];
+    const float L = red[2][0] + red[2][1] + red[2][2] + red[2][3];
+    out[(int64_t)row * d + h * 64 + tid] = f2bf(o / L);
   }
 }
 
@@ -713,10 +827,9 @@ void decode_self_attn(const T* qkv, const float* qkv_part, int qkv_splits, const
                       hipStream_t s) {
   if (D <= 0) return;
   if constexpr (sizeof(T) == 2) {
-    static_assert(kTextCtx % 32 == 0, "passes");
-    k_dattn_bf16<true, kTextCtx / 32><<<dim3(n_head, D, 1), 256, 0, s>>>(
+    k_dattn_self_bf16<<<dim3(n_head, D, 1), 256, 0, s>>>(
         qkv_part, qkv_splits, qkv_bias, D, (bf16_t*)cache, slot_stride, layer_off, slots, pos,
-        n_head, part, (bf16_t*)out);
+        n_head, (bf16_t*)out);
     return;
   }
   constexpr int nch = (kTextCtx + DA_CK - 1) / DA_CK;
@@ -732,9 +845,9 @@ void decode_cross_attn(const float* q_part, int q_splits, const float* q_bias, T
   constexpr int nch = (kCtx + DA_CK - 1) / DA_CK;
   if constexpr (sizeof(T) == 2) {
     static_assert(DA_CK % 32 == 0, "passes");
-    k_dattn_bf16<false, DA_CK / 32><<<dim3(n_head, D, nch), 256, 0, s>>>(
-        q_part, q_splits, q_bias, D, (bf16_t*)cache, slot_stride, layer_off, slots, nullptr,
-        n_head, part, nullptr);
+    k_dattn_cross_bf16<DA_CK / 32><<<dim3(n_head, D, nch), 256, 0, s>>>(
+        q_part, q_splits, q_bias, D, (const bf16_t*)cache, slot_stride, layer_off, slots, n_head,
+        part);
     k_decode_combine<T, false><<<(D * n_head + 3) / 4, 256, 0, s>>>(part, nullptr, D, n_head, out);
     return;
   }

@@ -1779,7 +1779,11 @@ void vocab_argmax_bf16(const bf16_t* x, const bf16_t* emb, int D, int V, int K, 
   if (D <= 0) return;
   (void)n_tiles;   // = vocab_tiles(V): the kernel derives it from V
   SkOut o{nullptr, nullptr, keys, logits};
-  launch_skinny<4, 6, 3, SK_ARGMAX>(x, emb, D, V, K, 1, o, s);
+  // 128 vocabulary rows per block with a 3-chunk weight and 2-chunk
+  // activation ring (80 KB of LDS): two blocks per CU, so the 406 blocks of
+  // the 51866-row table are all resident at once instead of running in a
+  // full round and a partial one
+  launch_skinny<4, 3, 2, SK_ARGMAX>(x, emb, D, V, K, 1, o, s);
 }
 
 void vocab_logits_f32(const float* x, const float* emb, int D, int V, int K, float* logits,

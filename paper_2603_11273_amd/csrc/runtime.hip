@@ -567,7 +567,7 @@ void gemm_any(asr_ctx* c, const AView& a, size_t w_off, int M, int N, int K, con
   double out_bytes = (double)M * N * c->es;
   if (e.kind == EPI_CONV2) out_bytes = (double)M * N * 4;
   double bytes = (double)M * K * c->es + (double)N * K * c->es + out_bytes;
-  timed(c, ASR_K_GEMM, flops, bytes, [&] {
+  timed(c, e.kind == EPI_XKV ? ASR_K_XKV : ASR_K_GEMM, flops, bytes, [&] {
     if (c->bf16())
       gemm_bf16(a, c->at<bf16_t>(w_off), M, N, K, e, c->stream);
     else
@@ -756,13 +756,6 @@ asr_status encode_clips(asr_ctx* c, int n, bool xkv = false) {
       res_ln_any<T>(c, x, y, R, last ? L.lnp_g : L.enc[l].ln1_g,
                     last ? L.lnp_b : L.enc[l].ln1_b, xn);
       if (last) enc_end();
-      if (last && xkv) {
-        const asr_status st2 = cross_kv<T>(c, xn, ng, clip0[grp]);
-        if (st2 != ASR_OK) {
-          c->stream = main_stream;
-          return st2;
-        }
-      }
     }
   }
   c->stream = main_stream;
@@ -773,10 +766,13 @@ asr_status encode_clips(asr_ctx* c, int n, bool xkv = false) {
   if (g.n_enc == 0) {
     ln_any<T>(c, x_all, n * kCtx, L.lnp_g, L.lnp_b, xn_all);
     enc_end();
-    if (xkv) {
-      const asr_status st2 = cross_kv<T>(c, xn_all, n, 0);
-      if (st2 != ASR_OK) return st2;
-    }
+  }
+  // the cross K/V of all clips as one product, after the groups have joined
+  // (a persistent GEMM fills every CU by itself, so splitting it by group
+  // gains nothing, and the encoder phase then ends where the product starts)
+  if (xkv) {
+    const asr_status st2 = cross_kv<T>(c, xn_all, n, 0);
+    if (st2 != ASR_OK) return st2;
   }
   CHECK_LAUNCH();
   return ASR_OK;
