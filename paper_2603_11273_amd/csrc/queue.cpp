@@ -37,14 +37,15 @@ void WaitQueue::admit_arrived(int64_t now_us) {
     std::pop_heap(later_.begin(), later_.end(), arrives_after);
     items_.push_back(later_.back());
     later_.pop_back();
-    std::push_heap(items_.begin(), items_.end(), cmp);
+    if (policy_ != HRRN) std::push_heap(items_.begin(), items_.end(), cmp);
   }
 }
 
 void WaitQueue::rebuild() {
-  for (auto& e : later_) items_.push_back(e);
-  later_.clear();
+  // Requests that have not arrived stay in the arrival heap: a policy switch
+  // re-keys them but does not move them into the policy's structure.
   for (auto& e : items_) e.job = job_of(e);
+  for (auto& e : later_) e.job = job_of(e);
   if (policy_ != HRRN)
     std::make_heap(items_.begin(), items_.end(),
                    [this](const QEntry& x, const QEntry& y) { return before(y, x, 0); });
@@ -60,21 +61,31 @@ void WaitQueue::set_policy(int policy, int32_t kappa_num, int32_t kappa_den) {
 void WaitQueue::push(QEntry e) {
   e.job = job_of(e);
   ids_.insert(e.id);
-  if (policy_ == HRRN) {
-    items_.push_back(e);
-  } else {
-    later_.push_back(e);
-    std::push_heap(later_.begin(), later_.end(), arrives_after);
+  later_.push_back(e);
+  std::push_heap(later_.begin(), later_.end(), arrives_after);
+}
+
+template <typename F>
+void WaitQueue::visit_arrived(int64_t now_us, F&& f) const {
+  for (const auto& e : items_)
+    if (e.arrival_us <= now_us) f(e);
+  // later_ is a min-heap by arrival: a node that has not arrived has no
+  // arrived descendant, so the walk stops there.
+  if (later_.empty() || later_.front().arrival_us > now_us) return;
+  std::vector<size_t> stack{0};
+  while (!stack.empty()) {
+    const size_t i = stack.back();
+    stack.pop_back();
+    if (later_[i].arrival_us > now_us) continue;
+    f(later_[i]);
+    if (2 * i + 1 < later_.size()) stack.push_back(2 * i + 1);
+    if (2 * i + 2 < later_.size()) stack.push_back(2 * i + 2);
   }
 }
 
 std::vector<int64_t> WaitQueue::rank(int64_t now_us) const {
   std::vector<const QEntry*> el;
-  el.reserve(size());
-  for (const auto& e : items_)
-    if (e.arrival_us <= now_us) el.push_back(&e);
-  for (const auto& e : later_)
-    if (e.arrival_us <= now_us) el.push_back(&e);
+  visit_arrived(now_us, [&](const QEntry& e) { el.push_back(&e); });
   std::sort(el.begin(), el.end(),
             [&](const QEntry* x, const QEntry* y) { return before(*x, *y, now_us); });
   std::vector<int64_t> ids;
@@ -86,6 +97,7 @@ std::vector<int64_t> WaitQueue::rank(int64_t now_us) const {
 std::vector<QEntry> WaitQueue::pop_batch(int64_t now_us, int max_n) {
   std::vector<QEntry> out;
   if (max_n <= 0) return out;
+  admit_arrived(now_us);
   if (policy_ == HRRN) {
     // ratios depend on now: a linear scan per pop
     while ((int)out.size() < max_n) {
@@ -100,7 +112,6 @@ std::vector<QEntry> WaitQueue::pop_batch(int64_t now_us, int max_n) {
       items_.pop_back();
     }
   } else {
-    admit_arrived(now_us);
     auto cmp = [this](const QEntry& x, const QEntry& y) { return before(y, x, 0); };
     std::vector<QEntry> later;                 // popped but not yet arrived (an earlier now)
     while ((int)out.size() < max_n && !items_.empty()) {
@@ -138,23 +149,19 @@ int64_t WaitQueue::min_arrival() const {
 
 int WaitQueue::eligible_count(int64_t now_us) const {
   int n = 0;
-  for (const auto& e : items_) n += e.arrival_us <= now_us;
-  for (const auto& e : later_) n += e.arrival_us <= now_us;
+  visit_arrived(now_us, [&](const QEntry&) { ++n; });
   return n;
 }
 
 void WaitQueue::max_ratio(int64_t now_us, int64_t* num, int64_t* den) const {
   int64_t bn = 0, bd = 1;
-  auto visit = [&](const QEntry& e) {
-    if (e.arrival_us > now_us) return;
+  visit_arrived(now_us, [&](const QEntry& e) {
     const int64_t n = now_us - e.arrival_us + e.job, d = e.job;
     if ((__int128)n * bd > (__int128)bn * d) {
       bn = n;
       bd = d;
     }
-  };
-  for (const auto& e : items_) visit(e);
-  for (const auto& e : later_) visit(e);
+  });
   *num = bn;
   *den = bd;
 }

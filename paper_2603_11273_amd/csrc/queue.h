@@ -59,16 +59,19 @@ class WaitQueue {
   bool before(const QEntry& a, const QEntry& b, int64_t now_us) const;
   void rebuild();
 
-  // FCFS/SJF keep requests that may not have arrived yet in a separate heap
-  // by arrival time and move them into the policy heap once a pop sees their
-  // arrival, so a queue holding many future requests (a simulation submits
-  // them all up front) still pops in logarithmic time.
+  // Every policy keeps requests that may not have arrived yet in a separate
+  // heap by arrival time and moves them into the policy's structure once a
+  // pop sees their arrival, so a queue holding many future requests (a
+  // simulation submits them all up front) pops, switches policy and scans for
+  // eligible requests in time that grows with the arrived ones only.
   void admit_arrived(int64_t now_us);
+  template <typename F>
+  void visit_arrived(int64_t now_us, F&& f) const;
 
   int policy_ = FCFS;
   int32_t kn_ = 0, kd_ = 0;
   std::vector<QEntry> items_;   // binary heap under FCFS/SJF, plain list under HRRN
-  std::vector<QEntry> later_;   // FCFS/SJF: min-heap by (arrival, id), not yet moved
+  std::vector<QEntry> later_;   // min-heap by (arrival, id), not yet moved
   std::unordered_set<int64_t> ids_;
 };
 
