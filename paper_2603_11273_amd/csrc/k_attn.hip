@@ -175,59 +175,79 @@ void k_flash_bf16(const bf16_t* __restrict__ qkv, const bf16_t* __restrict__ vt,
           if (key >= kCtx) s[kb][r] = -INFINITY;
         }
     }
-    float tmax = -INFINITY;
+    // probabilities of the tile against the current reference, packed to
+    // bf16 (the P V product's B operand), and their sum
+    uint32_t u[2][2][4];
+    float lt = 0.f;
+    auto probs = [&]() {
+      lt = 0.f;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, s[kb][r]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+        for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            // keys kb*32 + hf*16 + half*8 + 2i, +1: registers hf*8 + 2i, +1
+            u[kb][hf][i] = pack2_bf16(__builtin_amdgcn_exp2f(s[kb][hf * 8 + 2 * i]),
+                                      __builtin_amdgcn_exp2f(s[kb][hf * 8 + 2 * i + 1]));
+            lt = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u[kb][hf][i]), ones,
+                                                 lt, false);
+          }
+    };
+    probs();
     // Lazy reference: probabilities are exp2(s - m) with m = 0 as long as
     // every score of the wave stays within 2^6 of it, so the common case
     // needs no subtraction at all.  exp2(s - m) may then reach 2^64, which
     // fp32 sums and bf16 operands carry with unchanged relative precision
-    // (both reach 2^127); the final 1/l cancels the offset.  A first tile
-    // whose maximum lies outside [-64, 64] sets m to it; a later score more
-    // than 2^6 above m moves m up and rescales O and l.
-    if (t == 0) {
-      if (__any(fabsf(tmax) > 64.0f)) {            // 64 real keys: finite
-        asm volatile("");
-        m = tmax;
-        zref = false;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) s[kb][r] -= tmax;
-      }
-    } else if (__any(tmax > 64.0f)) {
+    // (both reach 2^127); the final 1/l cancels the offset.  The common case
+    // does not look for the tile's maximum either: a score more than 2^6
+    // above m (or +inf) makes its lane's probability sum exceed 2^64, and on
+    // the first tile a lane whose scores all lie far below 0 sums to less
+    // than 2^-64.  Only such tiles take the exact maximum: a first tile whose
+    // maximum lies outside [-64, 64] sets m to it; a later maximum more than
+    // 2^6 above m moves m up and rescales O and l; the tile's probabilities
+    // are then recomputed.
+    if (__any(lt > 0x1p64f) || (t == 0 && __any(lt < 0x1p-64f))) {
       asm volatile("");
-      const float shift = fmaxf(tmax, 0.f);
-      const float alpha = __builtin_amdgcn_exp2f(-shift);
-      m += shift;
-      zref = false;
-      l *= alpha;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        o0[r] *= alpha;
-        o1[r] *= alpha;
-      }
+      float tmax = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) s[kb][r] -= shift;
+        for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, s[kb][r]);
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+      if (t == 0) {
+        if (__any(fabsf(tmax) > 64.0f)) {          // 64 real keys: finite
+          m = tmax;
+          zref = false;
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) s[kb][r] -= tmax;
+        }
+      } else if (__any(tmax > 64.0f)) {
+        const float shift = fmaxf(tmax, 0.f);
+        const float alpha = __builtin_amdgcn_exp2f(-shift);
+        m += shift;
+        zref = false;
+        l *= alpha;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          o0[r] *= alpha;
+          o1[r] *= alpha;
+        }
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) s[kb][r] -= shift;
+      }
+      probs();
     }
+    l += lt;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
-        // keys kb*32 + hf*16 + half*8 .. +8: registers hf*8 .. hf*8+7
-        uint32_t u[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          u[i] = pack2_bf16(__builtin_amdgcn_exp2f(s[kb][hf * 8 + 2 * i]),
-                            __builtin_amdgcn_exp2f(s[kb][hf * 8 + 2 * i + 1]));
-          l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u[i]), ones, l, false);
-        }
-        const bf16x8 pb = as_bf16x8(uint4{u[0], u[1], u[2], u[3]});
+        const bf16x8 pb = as_bf16x8(uint4{u[kb][hf][0], u[kb][hf][1], u[kb][hf][2], u[kb][hf][3]});
         o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(kb, hf, l32), pb, o0, 0, 0, 0);
         o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(kb, hf, 32 + l32), pb, o1, 0, 0, 0);
       }
