@@ -180,7 +180,7 @@ void k_flash_bf16(const bf16_t* __restrict__ qkv, const bf16_t* __restrict__ vt,
     uint32_t u[2][2][4];
     float lt = 0.f;
     auto probs = [&]() {
-      lt = 0.f;
+      float ls[4] = {0.f, 0.f, 0.f, 0.f};          // four independent sum chains
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -190,9 +190,10 @@ void k_flash_bf16(const bf16_t* __restrict__ qkv, const bf16_t* __restrict__ vt,
             // keys kb*32 + hf*16 + half*8 + 2i, +1: registers hf*8 + 2i, +1
             u[kb][hf][i] = pack2_bf16(__builtin_amdgcn_exp2f(s[kb][hf * 8 + 2 * i]),
                                       __builtin_amdgcn_exp2f(s[kb][hf * 8 + 2 * i + 1]));
-            lt = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u[kb][hf][i]), ones,
-                                                 lt, false);
+            ls[i] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u[kb][hf][i]),
+                                                    ones, ls[i], false);
           }
+      lt = (ls[0] + ls[1]) + (ls[2] + ls[3]);
     };
     probs();
     // Lazy reference: probabilities are exp2(s - m) with m = 0 as long as
