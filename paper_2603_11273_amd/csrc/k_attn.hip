@@ -73,11 +73,26 @@ void k_flash_bf16(const bf16_t* __restrict__ qkv, const bf16_t* __restrict__ vt,
   __shared__ __attribute__((aligned(16))) bf16_t Ks[S][FP_KT * 64];   // [key][dim]
   __shared__ __attribute__((aligned(16))) bf16_t Vs[S][64 * FP_KT];   // [dim][key]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int h = blockIdx.y, b = blockIdx.z;
+  // XCD-aware work order: the hardware deals blocks round-robin to the 8
+  // XCDs in dispatch order (x fastest), so block i runs on XCD i % 8.  Each
+  // XCD takes a contiguous range of (query block, head, clip) work items,
+  // query block fastest, so the query blocks of one (clip, head) share an
+  // L2 and its K and V^T tiles are fetched from beyond it about once.
+  int qb, h, b;
+  {
+    const int nqb = gridDim.x, nh = gridDim.y;
+    const int total = nqb * nh * (int)gridDim.z;
+    const int lin = (int)blockIdx.x + nqb * ((int)blockIdx.y + nh * (int)blockIdx.z);
+    const int per = total / 8, rem = total % 8, xcd = lin % 8;
+    const int w = xcd * per + min(xcd, rem) + lin / 8;
+    qb = w % nqb;
+    h = (w / nqb) % nh;
+    b = w / (nqb * nh);
+  }
   const int d = n_head * 64, ld3 = 3 * d;
   const bf16_t* base = qkv + (int64_t)b * kCtx * ld3;
   const int half = lane >> 5, l32 = lane & 31;
-  const int q = blockIdx.x * (FP_NW * 32) + wave * 32 + l32;   // this lane's query
+  const int q = qb * (FP_NW * 32) + wave * 32 + l32;   // this lane's query
   constexpr int NT = (kCtx + FP_KT - 1) / FP_KT;
 
   // Q fragments (B operand of S^T): dims kk*16 + half*8 .. +8 of query q
