@@ -109,11 +109,14 @@ int vocab_tiles(int V);
 template <typename T>
 void layer_norm(const float* x, int rows, int d, const float* g, const float* b, T* out,
                 hipStream_t s);
-// Residual add fused with the LayerNorm that follows it: x += y, out = LN(x)
-// (the residual branch y in storage type T, the stream x in float32).
+// Residual add fused with the LayerNorm that follows it, the branches in
+// storage type T (rows ldy elements apart), the stream x in float32:
+//   y2 == nullptr, store:  x += y1,            out = LN(x)
+//   y2 == nullptr, !store: out = LN(x + y1)    (x unchanged)
+//   y2 != nullptr:         x = (x + y1) + y2,  out = LN(x)
 template <typename T>
-void residual_layer_norm(float* x, const T* y, int rows, int d, const float* g,
-                         const float* b, T* out, hipStream_t s);
+void residual_layer_norm(float* x, const T* y1, const T* y2, int64_t ldy, bool store, int rows,
+                         int d, const float* g, const float* b, T* out, hipStream_t s);
 
 // Writes given float32 operands [B*1500][d] where the attention kernels read
 // them (which: 0 = q, scaled by qmul; 1 = k; 2 = v, transposed into vt for

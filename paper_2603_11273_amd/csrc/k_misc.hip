@@ -132,13 +132,20 @@ __device__ __forceinline__ float4 ld4<bf16_t>(const bf16_t* p) {
                      __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u));
 }
 
-// All of a row's loads (x, y, gain, bias) are issued before the first
+// Residual modes of the LayerNorm kernels: LN_PLAIN normalises x;
+// LN_RES adds one branch (x += y1, stored) first; LN_RES_TEMP normalises
+// x + y1 without storing the sum; LN_RES2 adds two branches in order
+// (x = (x + y1) + y2, stored).  Branch rows are ldy elements apart.
+enum LnMode : int { LN_PLAIN = 0, LN_RES = 1, LN_RES_TEMP = 2, LN_RES2 = 3 };
+
+// All of a row's loads (x, branches, gain, bias) are issued before the first
 // store, and the reductions stay in VALU lanes (DPP and lane swaps): the
 // row's two passes over HBM then overlap instead of alternating with waits.
-template <typename T, int Q, bool RES>
+template <typename T, int Q, int MODE>
 __global__ __launch_bounds__(256) void k_layer_norm(float* __restrict__ x,
-                                                    const T* __restrict__ y, int rows,
-                                                    const float* __restrict__ g,
+                                                    const T* __restrict__ y1,
+                                                    const T* __restrict__ y2, int64_t ldy,
+                                                    int rows, const float* __restrict__ g,
                                                     const float* __restrict__ b,
                                                     T* __restrict__ out) {
   constexpr int d = Q * 256;
@@ -146,12 +153,13 @@ __global__ __launch_bounds__(256) void k_layer_norm(float* __restrict__ x,
   int lane = threadIdx.x & 63;
   if (row >= rows) return;
   float* xr = x + (int64_t)row * d;
-  float4 v[Q], t[Q], gg[Q], bb[Q];
+  float4 v[Q], t[Q], t2[Q], gg[Q], bb[Q];
 #pragma unroll
   for (int i = 0; i < Q; ++i) {
     const int e = (lane + 64 * i) * 4;
     v[i] = *(const float4*)(xr + e);
-    if constexpr (RES) t[i] = ld4<T>(y + (int64_t)row * d + e);
+    if constexpr (MODE != LN_PLAIN) t[i] = ld4<T>(y1 + (int64_t)row * ldy + e);
+    if constexpr (MODE == LN_RES2) t2[i] = ld4<T>(y2 + (int64_t)row * ldy + e);
   }
 #pragma unroll
   for (int i = 0; i < Q; ++i) {
@@ -162,10 +170,11 @@ __global__ __launch_bounds__(256) void k_layer_norm(float* __restrict__ x,
   float s = 0.f;
 #pragma unroll
   for (int i = 0; i < Q; ++i) {
-    if constexpr (RES) {
+    if constexpr (MODE != LN_PLAIN)
       v[i] = make_float4(v[i].x + t[i].x, v[i].y + t[i].y, v[i].z + t[i].z, v[i].w + t[i].w);
-      *(float4*)(xr + (lane + 64 * i) * 4) = v[i];
-    }
+    if constexpr (MODE == LN_RES2)
+      v[i] = make_float4(v[i].x + t2[i].x, v[i].y + t2[i].y, v[i].z + t2[i].z, v[i].w + t2[i].w);
+    if constexpr (MODE == LN_RES || MODE == LN_RES2) *(float4*)(xr + (lane + 64 * i) * 4) = v[i];
     s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
   }
   float mean = wave_sum_lanes(s) * (1.0f / d);
@@ -185,60 +194,79 @@ __global__ __launch_bounds__(256) void k_layer_norm(float* __restrict__ x,
   }
 }
 
-// Any d that is a multiple of 64: two passes over global memory.
-template <typename T, bool RES>
-__global__ __launch_bounds__(256) void k_layer_norm_any(float* x, const T* y, int rows,
-                                                        int d, const float* g, const float* b,
-                                                        T* out) {
+// Any d that is a multiple of 64: two passes over global memory (the sum
+// is formed in the same order as above; LN_RES_TEMP recomputes it).
+template <typename T, int MODE>
+__global__ __launch_bounds__(256) void k_layer_norm_any(float* x, const T* y1, const T* y2,
+                                                        int64_t ldy, int rows, int d,
+                                                        const float* g, const float* b, T* out) {
   int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   int lane = threadIdx.x & 63;
   if (row >= rows) return;
   float* xr = x + (int64_t)row * d;
+  auto val = [&](int e) {
+    float v = xr[e];
+    if constexpr (MODE != LN_PLAIN) v += St<T>::ld(y1, (int64_t)row * ldy + e);
+    if constexpr (MODE == LN_RES2) v += St<T>::ld(y2, (int64_t)row * ldy + e);
+    return v;
+  };
   float s = 0.f;
   for (int e = lane; e < d; e += 64) {
-    if constexpr (RES) xr[e] += St<T>::ld(y, (int64_t)row * d + e);
-    s += xr[e];
+    const float v = val(e);
+    if constexpr (MODE == LN_RES || MODE == LN_RES2) xr[e] = v;
+    s += v;
   }
   float mean = wave_sum(s) / d;
+  auto cur = [&](int e) {
+    if constexpr (MODE == LN_RES_TEMP) return val(e);
+    else return xr[e];
+  };
   float q = 0.f;
   for (int e = lane; e < d; e += 64) {
-    float t = xr[e] - mean;
+    float t = cur(e) - mean;
     q += t * t;
   }
   float rstd = rsqrtf(wave_sum(q) / d + 1e-5f);
   T* o = out + (int64_t)row * d;
-  for (int e = lane; e < d; e += 64) St<T>::st(o, e, (xr[e] - mean) * rstd * g[e] + b[e]);
+  for (int e = lane; e < d; e += 64) St<T>::st(o, e, (cur(e) - mean) * rstd * g[e] + b[e]);
 }
 
-template <typename T, bool RES>
-static void layer_norm_launch(float* x, const T* y, int rows, int d, const float* g,
-                              const float* b, T* out, hipStream_t s) {
+template <typename T, int MODE>
+static void layer_norm_launch(float* x, const T* y1, const T* y2, int64_t ldy, int rows, int d,
+                              const float* g, const float* b, T* out, hipStream_t s) {
   if (rows <= 0) return;
   dim3 grid((rows + 3) / 4);
   switch (d) {
-    case 512: k_layer_norm<T, 2, RES><<<grid, 256, 0, s>>>(x, y, rows, g, b, out); break;
-    case 768: k_layer_norm<T, 3, RES><<<grid, 256, 0, s>>>(x, y, rows, g, b, out); break;
-    case 1024: k_layer_norm<T, 4, RES><<<grid, 256, 0, s>>>(x, y, rows, g, b, out); break;
-    case 1280: k_layer_norm<T, 5, RES><<<grid, 256, 0, s>>>(x, y, rows, g, b, out); break;
-    default: k_layer_norm_any<T, RES><<<grid, 256, 0, s>>>(x, y, rows, d, g, b, out); break;
+    case 512: k_layer_norm<T, 2, MODE><<<grid, 256, 0, s>>>(x, y1, y2, ldy, rows, g, b, out); break;
+    case 768: k_layer_norm<T, 3, MODE><<<grid, 256, 0, s>>>(x, y1, y2, ldy, rows, g, b, out); break;
+    case 1024: k_layer_norm<T, 4, MODE><<<grid, 256, 0, s>>>(x, y1, y2, ldy, rows, g, b, out); break;
+    case 1280: k_layer_norm<T, 5, MODE><<<grid, 256, 0, s>>>(x, y1, y2, ldy, rows, g, b, out); break;
+    default: k_layer_norm_any<T, MODE><<<grid, 256, 0, s>>>(x, y1, y2, ldy, rows, d, g, b, out); break;
   }
 }
 
 template <typename T>
 void layer_norm(const float* x, int rows, int d, const float* g, const float* b, T* out,
                 hipStream_t s) {
-  layer_norm_launch<T, false>(const_cast<float*>(x), nullptr, rows, d, g, b, out, s);
+  layer_norm_launch<T, LN_PLAIN>(const_cast<float*>(x), nullptr, nullptr, 0, rows, d, g, b, out,
+                                 s);
 }
 
 template <typename T>
-void residual_layer_norm(float* x, const T* y, int rows, int d, const float* g,
-                         const float* b, T* out, hipStream_t s) {
-  layer_norm_launch<T, true>(x, y, rows, d, g, b, out, s);
+void residual_layer_norm(float* x, const T* y1, const T* y2, int64_t ldy, bool store, int rows,
+                         int d, const float* g, const float* b, T* out, hipStream_t s) {
+  if (y2)
+    layer_norm_launch<T, LN_RES2>(x, y1, y2, ldy, rows, d, g, b, out, s);
+  else if (store)
+    layer_norm_launch<T, LN_RES>(x, y1, nullptr, ldy, rows, d, g, b, out, s);
+  else
+    layer_norm_launch<T, LN_RES_TEMP>(x, y1, nullptr, ldy, rows, d, g, b, out, s);
 }
-template void residual_layer_norm<float>(float*, const float*, int, int, const float*,
-                                         const float*, float*, hipStream_t);
-template void residual_layer_norm<bf16_t>(float*, const bf16_t*, int, int, const float*,
-                                          const float*, bf16_t*, hipStream_t);
+template void residual_layer_norm<float>(float*, const float*, const float*, int64_t, bool, int,
+                                         int, const float*, const float*, float*, hipStream_t);
+template void residual_layer_norm<bf16_t>(float*, const bf16_t*, const bf16_t*, int64_t, bool,
+                                          int, int, const float*, const float*, bf16_t*,
+                                          hipStream_t);
 template void layer_norm<float>(const float*, int, int, const float*, const float*, float*,
                                 hipStream_t);
 template void layer_norm<bf16_t>(const float*, int, int, const float*, const float*, bf16_t*,

@@ -583,13 +583,17 @@ void ln_any(asr_ctx* c, const float* x, int rows, size_t g, size_t b, T* out) {
   });
 }
 
-// x += y, then out = LayerNorm(x): the residual add of a block fused with the
-// LayerNorm that follows it.
+// The residual adds of a block fused with the LayerNorm that follows them
+// (branch rows ldy elements apart): with y2, x = (x + y1) + y2 is stored and
+// normalised; without, LayerNorm(x + y1) is formed and x is left as it was.
 template <typename T>
-void res_ln_any(asr_ctx* c, float* x, const T* y, int rows, size_t g, size_t b, T* out) {
+void res_ln_any(asr_ctx* c, float* x, const T* y1, const T* y2, int64_t ldy, int rows, size_t g,
+                size_t b, T* out) {
   const int d = c->cfg.d_model;
-  timed(c, ASR_K_LN, 9.0 * rows * d, (double)rows * d * (8 + 2 * c->es), [&] {
-    residual_layer_norm<T>(x, y, rows, d, c->at<float>(g), c->at<float>(b), out, c->stream);
+  const double bytes = y2 ? (double)rows * d * (8 + 3 * c->es) : (double)rows * d * (4 + 2 * c->es);
+  timed(c, ASR_K_LN, 9.0 * rows * d, bytes, [&] {
+    residual_layer_norm<T>(x, y1, y2, ldy, y2 != nullptr, rows, d, c->at<float>(g),
+                           c->at<float>(b), out, c->stream);
   });
 }
 
@@ -665,11 +669,14 @@ asr_status encode_clips(asr_ctx* c, int n, bool xkv = false) {
       T* att = att_all + r0 * d;
       T* hid = hid_all + r0 * F;
       // The residual branches (attention out-projection, FC2) are written in
-      // the storage type to y, which borrows the group's QKV rows (dead once
-      // attention has run); the LayerNorm kernel that follows adds y into the
-      // float32 stream, as a model stored in bf16 adds its bf16 branch
-      // outputs to the residual.
-      T* y = qkv;
+      // the storage type to ya and yf, which borrow the group's QKV rows
+      // (dead once attention has run; rows 3d apart), and are added into the
+      // float32 stream by the LayerNorm kernels that follow, as a model
+      // stored in bf16 adds its bf16 branch outputs to the residual.  The
+      // first LayerNorm normalises x + ya without storing it; the second
+      // stores x = (x + ya) + yf (the same sums, one write of x per layer).
+      T* ya = qkv;
+      T* yf = qkv + d;
       if (l == 0) {
         // conv1: rows t of clip g read padded mel rows t .. t+2 (positions t-1 .. t+1)
         {
@@ -727,12 +734,12 @@ asr_status encode_clips(asr_ctx* c, int n, bool xkv = false) {
         AView a{att, d, 0, R};
         Epilogue e{};
         e.kind = EPI_STORE;
-        e.out = y;
-        e.ldc = d;
+        e.out = ya;
+        e.ldc = 3 * d;
         e.bias = c->at<float>(w.o_b);
         gemm_any<T>(c, a, w.o_w, R, d, d, e);
       }
-      res_ln_any<T>(c, x, y, R, w.ln2_g, w.ln2_b, xn);
+      res_ln_any<T>(c, x, ya, nullptr, 3 * d, R, w.ln2_g, w.ln2_b, xn);
       {
         AView a{xn, d, 0, R};
         Epilogue e{};
@@ -746,14 +753,14 @@ asr_status encode_clips(asr_ctx* c, int n, bool xkv = false) {
         AView a{hid, F, 0, R};
         Epilogue e{};
         e.kind = EPI_STORE;
-        e.out = y;
-        e.ldc = d;
+        e.out = yf;
+        e.ldc = 3 * d;
         e.bias = c->at<float>(w.fc2_b);
         gemm_any<T>(c, a, w.fc2_w, R, d, F, e);
       }
       // the next LayerNorm: the next layer's LN_1, or ln_post after the last layer
       const bool last = l == g.n_enc;
-      res_ln_any<T>(c, x, y, R, last ? L.lnp_g : L.enc[l].ln1_g,
+      res_ln_any<T>(c, x, ya, yf, 3 * d, R, last ? L.lnp_g : L.enc[l].ln1_g,
                     last ? L.lnp_b : L.enc[l].ln1_b, xn);
       if (last) enc_end();
     }

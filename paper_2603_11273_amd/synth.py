@@ -361,7 +361,7 @@ def kv_lengths(seed: int, n: int, lo: int = 10, hi: int = 400) -> np.ndarray:
     return rng.integers(lo, hi + 1, size=n, dtype=np.int64).astype(np.int32)
 
 
-ATTENTION_CASES = ("small", "first_tile_large", "late_large", "very_negative")
+ATTENTION_CASES = ("small", "first_tile_large", "late_large", "late_huge", "very_negative")
 
 
 def attention_operands(seed: int, n: int, d_model: int, case: str):
@@ -372,9 +372,12 @@ def attention_operands(seed: int, n: int, d_model: int, case: str):
     `case`, a shared +-1 pattern u per head (|u|^2 = 64): 'small' has none;
     'first_tile_large' adds u to the queries and 1.5 u to keys 0..63;
     'late_large' adds u to the queries and 1.5 u to keys 900..963;
+    'late_huge' adds u to the queries and 2.5 u to keys 900..963;
     'very_negative' adds u to the queries and -1.5 u to every key.  With q
-    read in the exp2 domain, the structured keys score about +-96 (the rest
-    stay within a few units), which moves the kernel's softmax reference."""
+    read in the exp2 domain, the structured keys score about +-96 (+160 for
+    'late_huge', past the 2^128 range of exp2 in fp32 against a reference
+    of 0; the rest stay within a few units), which moves the kernel's
+    softmax reference."""
     assert case in ATTENTION_CASES
     rng = np.random.default_rng([seed, 29, ATTENTION_CASES.index(case)])
     shp = (n, N_AUDIO_CTX, d_model)
@@ -388,6 +391,8 @@ def attention_operands(seed: int, n: int, d_model: int, case: str):
             k[:, 0:64] += 1.5 * u
         elif case == "late_large":
             k[:, 900:964] += 1.5 * u
+        elif case == "late_huge":
+            k[:, 900:964] += 2.5 * u
         else:
             k += -1.5 * u
     return q, k, v
