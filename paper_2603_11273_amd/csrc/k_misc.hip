@@ -376,11 +376,12 @@ template <class Clips>
 __global__ __launch_bounds__(256) void k_log_mel(Clips clips, int n_clips, int n_mels,
                                                  MelTables tb, float* mel_raw,
                                                  float* group_max) {
-  // segment samples and the power spectrum [MEL_FR][kBins + 3] (16 floats
-  // of slack: a filter's bin window may run past the last row's bin 200)
+  // segment samples and the power spectrum [MEL_FR][kBins + 3] (32 floats
+  // of slack: a filter's aligned bin window may run past the last row's
+  // bin 200, by at most 19 bins)
   constexpr int SEG_SLOTS = MEL_PT * 256;
   __shared__ float seg[SEG_SLOTS];
-  __shared__ float pwbuf[MEL_FR * (kBins + 3) + 16];
+  __shared__ __attribute__((aligned(16))) float pwbuf[MEL_FR * (kBins + 3) + 32];
   __shared__ float2 bst[MEL_FR * MEL_FST];               // stage-1 output [f][n2][k1]
   __shared__ float fbw[2 * kBins];                       // packed filter weights (bins past 16)
   __shared__ float red[4];
@@ -394,7 +395,7 @@ __global__ __launch_bounds__(256) void k_log_mel(Clips clips, int n_clips, int n
   // slack after the last) is never written by stage 2 and stays zero, so
   // a filter's reads past its own bins multiply a finite value (or zero) by
   // its zero weights, as the dense filterbank product would
-  for (int i = tid; i < MEL_FR * (kBins + 3) + 16; i += 256) pwbuf[i] = 0.0f;
+  for (int i = tid; i < MEL_FR * (kBins + 3) + 32; i += 256) pwbuf[i] = 0.0f;
   for (int i = tid; i < n_clips; i += 256) {
     const int64_t n = clips.len(i);
     c_ptr[i] = n > 0 ? clips.ptr(i) : tb.window;   // a clip without samples reads the window
@@ -418,16 +419,24 @@ __global__ __launch_bounds__(256) void k_log_mel(Clips clips, int n_clips, int n
   // Mel role: filter m = tid % n_mels for frames tid / n_mels + j * mel_fs
   // (threads past mel_fs * n_mels idle), with the filter's first 16 weights
   // (zero past its end); filters past 16 bins (below 64 mels) take the rest
-  // from LDS.
+  // from LDS.  The power rows are read in aligned float4s from the bin
+  // m_k0 - m_sh (the multiple of 4 at or below the filter's first bin), so
+  // the weight registers start m_sh zeros early: the extra bins add
+  // fma(0, p, acc) = acc, the products and their order are unchanged.
   const int mel_fs = 256 / n_mels;   // >= 2
   const int mm = tid % n_mels, m_f = tid / n_mels;
   const bool m_on = tid < mel_fs * n_mels;
   const int m_k0 = tb.fb_range[3 * mm], m_cnt = m_on ? tb.fb_range[3 * mm + 1] : 0;
   const int m_off = tb.fb_range[3 * mm + 2];
-  float m_w[16];
+  const int m_sh = m_k0 & 3;
+  float m_w[20];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) m_w[i] = i < m_cnt ? tb.fb[m_off + i] : 0.0f;
-  int wave_cnt = m_cnt;
+  for (int i = 0; i < 20; ++i) {
+    const int j = i - m_sh;
+    m_w[i] = j >= 0 && j < m_cnt && j < 16 ? tb.fb[m_off + j] : 0.0f;
+  }
+  // float4 reads a frame needs: the wave's widest aligned window
+  int wave_cnt = m_on ? (m_sh + min(m_cnt, 16) + 3) / 4 : 0;
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) wave_cnt = max(wave_cnt, __shfl_xor(wave_cnt, o, 64));
   wave_cnt = __builtin_amdgcn_readfirstlane(wave_cnt);
@@ -440,7 +449,9 @@ __global__ __launch_bounds__(256) void k_log_mel(Clips clips, int n_clips, int n
   // that they completed and would otherwise wait for every load and store
   // in flight at each of them.
 #pragma unroll
-  for (int i = 0; i < 16; ++i) asm volatile("" : "+v"(s1_win[i]), "+v"(m_w[i]));
+  for (int i = 0; i < 16; ++i) asm volatile("" : "+v"(s1_win[i]));
+#pragma unroll
+  for (int i = 0; i < 20; ++i) asm volatile("" : "+v"(m_w[i]));
 #pragma unroll
   for (int i = 1; i < MEL_COLS; ++i) asm volatile("" : "+v"(tw_c[i]), "+v"(tw_s[i]));
 
@@ -584,24 +595,31 @@ __global__ __launch_bounds__(256) void k_log_mel(Clips clips, int n_clips, int n
     __syncthreads();
 
     // filterbank, log10 with the 1e-10 floor, the group's maximum; each
-    // frame reads NB bins from the filter's first, NB the widest filter of
-    // the wave rounded up (one straight-line variant per width)
+    // frame reads NB4 aligned float4s of bins from the filter's aligned
+    // start, NB4 the wave's widest window (one straight-line variant per
+    // width)
     float local_max = -INFINITY;
     float* const out_g = mel_raw + ((int64_t)clip * kFrames + f0 + m_f) * n_mels + mm;
     auto filters = [&](auto nb) {
-      constexpr int NB = decltype(nb)::value;
+      constexpr int NB4 = decltype(nb)::value;
 #pragma unroll
       for (int j = 0; j < MEL_FR / 2; ++j) {   // mel_fs >= 2: at most 8 frames per thread
         const int f = m_f + j * mel_fs;
         if (!m_on || f >= MEL_FR || f0 + f >= kFrames) continue;
         const float* prow = pw[f] + m_k0;
-        float v[NB];
+        const float4* prow4 = (const float4*)(pw[f] + (m_k0 - m_sh));
+        float4 v[NB4];
 #pragma unroll
-        for (int i = 0; i < NB; ++i) v[i] = prow[i];
-        // bins past the lane's own filter carry zero weight
+        for (int i = 0; i < NB4; ++i) v[i] = prow4[i];
+        // bins outside the lane's own filter carry zero weight
         float acc = 0.f;
 #pragma unroll
-        for (int i = 0; i < NB; ++i) acc = fmaf(m_w[i], v[i], acc);
+        for (int i = 0; i < NB4; ++i) {
+          acc = fmaf(m_w[4 * i], v[i].x, acc);
+          acc = fmaf(m_w[4 * i + 1], v[i].y, acc);
+          acc = fmaf(m_w[4 * i + 2], v[i].z, acc);
+          acc = fmaf(m_w[4 * i + 3], v[i].w, acc);
+        }
         for (int i = 16; i < m_cnt; ++i) acc = fmaf(fbw[m_off + i], prow[i], acc);
         // log10 as log2 times log10(2) (the argument is a normal float)
         const float L = __builtin_amdgcn_logf(fmaxf(acc, 1e-10f)) * 0.30102999566398120f;
@@ -609,14 +627,11 @@ __global__ __launch_bounds__(256) void k_log_mel(Clips clips, int n_clips, int n
         local_max = fmaxf(local_max, L);
       }
     };
-    if (wave_cnt <= 2) filters(std::integral_constant<int, 2>());
+    if (wave_cnt <= 1) filters(std::integral_constant<int, 1>());
+    else if (wave_cnt <= 2) filters(std::integral_constant<int, 2>());
+    else if (wave_cnt <= 3) filters(std::integral_constant<int, 3>());
     else if (wave_cnt <= 4) filters(std::integral_constant<int, 4>());
-    else if (wave_cnt <= 6) filters(std::integral_constant<int, 6>());
-    else if (wave_cnt <= 8) filters(std::integral_constant<int, 8>());
-    else if (wave_cnt <= 10) filters(std::integral_constant<int, 10>());
-    else if (wave_cnt <= 12) filters(std::integral_constant<int, 12>());
-    else if (wave_cnt <= 14) filters(std::integral_constant<int, 14>());
-    else filters(std::integral_constant<int, 16>());
+    else filters(std::integral_constant<int, 5>());
     local_max = wave_max(local_max);
     if ((tid & 63) == 0) red[tid >> 6] = local_max;
     __syncthreads();
