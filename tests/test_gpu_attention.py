@@ -41,3 +41,23 @@ def test_attention_matches_oracle(name, case):
         worst = max(worst, e)
         assert e <= ATT_TOL[shape.dtype], f"clip {b}: rel err {e:.3e}"
     print(f"attention {name} {case}: worst rel err {worst:.3e}")
+
+
+@pytest.mark.parametrize("n", [1, 3])
+def test_attention_block_count_not_a_multiple_of_eight(n):
+    """The kernel deals its (query block, head, clip) work items to the 8
+    XCDs in contiguous ranges; with 6 heads and 1 or 3 clips the block count
+    (36, 108) leaves a remainder, so the first XCDs take one item more.
+    Every item must still be computed exactly once."""
+    shape = synth.reduced_shape(synth.SHAPES["tiny"], 1, 0, dtype="bf16")
+    assert shape.n_head == 6
+    seed = 20260351 + n
+    ctx = make_context(shape, seed, max_slots=0, max_prefill=n, max_decode=0)
+    q, k, v = synth.attention_operands(seed, n, shape.d_model, "small")
+    got = ctx.debug_attention(q, k, v)
+    assert np.all(np.isfinite(got))
+    qn = q.astype(np.float64) * (8.0 / math.log2(math.e))
+    for b in range(n):
+        ref = OW.attention(qn[b], k[b].astype(np.float64), v[b].astype(np.float64), shape.n_head)
+        e = rel_err(got[b], ref)
+        assert e <= ATT_TOL["bf16"], f"clip {b}: rel err {e:.3e}"
