@@ -47,13 +47,16 @@ def test_logmel_matches_oracle(n_mels):
 # ----------------------------------------------------------------------------
 # encoder (mel -> stem -> layers -> ln_post)
 # ----------------------------------------------------------------------------
-@pytest.mark.parametrize("name,n_enc,lengths", [
-    ("tiny", 4, [64000, 480000]),          # fp32 path, full depth
-    ("base", 2, [96000, 16000, 480000]),   # bf16 path
-    ("large-v3", 1, [480000]),             # 128 mels, d = 1280
+@pytest.mark.parametrize("name,n_enc,lengths,dtype", [
+    ("tiny", 4, [64000, 480000], None),          # fp32 path, full depth
+    ("base", 2, [96000, 16000, 480000], None),   # bf16 path
+    ("large-v3", 1, [480000], None),             # 128 mels, d = 1280
+    # bf16 at d = 384: the LayerNorm kernels' general-width path with both
+    # residual modes, and a flash-attention grid that is not a multiple of 8
+    ("tiny", 2, [32000, 480000, 7], "bf16"),
 ])
-def test_encoder_matches_oracle(name, n_enc, lengths):
-    shape = synth.reduced_shape(synth.SHAPES[name], n_enc, 0)
+def test_encoder_matches_oracle(name, n_enc, lengths, dtype):
+    shape = synth.reduced_shape(synth.SHAPES[name], n_enc, 0, dtype=dtype)
     seed = 101
     ctx = make_context(shape, seed, max_slots=0, max_prefill=len(lengths), max_decode=0)
     clips = _clips(seed, lengths)
